@@ -1,0 +1,183 @@
+/*
+ * moe.h - C ABI of the mixed-precision MoE layer library for AMD MI355X
+ * (gfx950).
+ *
+ * The library runs one sparse MoE layer (HOBBIT, arXiv 2411.01433):
+ *
+ *   y = sum_{i<K} G(x)_{e_i} * E_{e_i}(x)                        (Eq. 1)
+ *
+ * where G is a linear gate followed by top-k and a softmax over the K
+ * selected logits (Section 2.1; "normalised" gate values, Section 3.2),
+ * and E is a SwiGLU expert  E(x) = W2 (silu(W1 x) * (W3 x)).  Each expert
+ * carries a precision tag standing for its state in the expert cache.  A
+ * resident expert runs at the precision it is held in; for a cache-miss
+ * expert the token-level rule of Section 3.2 (Eq. 2) chooses per token:
+ * rank the K gate values in descending order, score s_i = sum of the gate
+ * values ranked above slot i (s_0 = 0), then
+ *   s <= t1       -> full precision (fp16)
+ *   t1 < s <= t2  -> low-precision copy (int4 or int2, from the tag)
+ *   s > t2        -> skipped (the term is dropped, no renormalisation)
+ * and the top-ranked expert always runs at full precision.
+ *
+ * Low-precision copies (Section 2.2, Section 4.1 "Configurations") are
+ * symmetric, group-wise along the input dimension, group = 32, one fp16
+ * scale per group:  s = fp16_rne(max|w| / qmax),  q = clamp(rne(w / s),
+ * -2^(b-1), qmax),  qmax = 2^(b-1) - 1;  stored offset-binary u = q + 2^(b-1),
+ * element j of a row at bit b*(j mod 8/b) of byte j*b/8.
+ *
+ * Conventions for every entry point
+ *  - Pointers documented "device" are HIP device pointers on the current
+ *    device; "host" pointers are ordinary process memory.
+ *  - Matrices are row-major.  Expert weights use the [out, in] layout:
+ *    W1, W3: [d_ff, d_model]; W2: [d_model, d_ff]; the gate Wg: [E, d_model].
+ *  - fp16 = IEEE binary16; fp32 = IEEE binary32.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Work is enqueued asynchronously on it; no entry point synchronises the
+ *    host except moe_layer_init, moe_layer_destroy and moe_set_expert_
+ *    precision when it has to allocate a low-precision copy.
+ *  - Argument errors are detected before any work is enqueued and return
+ *    MOE_EINVAL with nothing enqueued.  A failing HIP call returns MOE_EHIP;
+ *    a device fault of earlier work surfaces as MOE_EHIP at a later call.
+ *  - moe_last_error() returns a thread-local description of the last
+ *    failure on the calling thread.
+ *  - No C++ exception crosses this interface.
+ *  - One handle must not be used from two streams concurrently (it owns a
+ *    single workspace).
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct moe_layer* moe_layer_t;
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_EINVAL = -1,       /* bad argument; nothing was enqueued */
+    MOE_ENOMEM = -2,       /* device or host allocation failed */
+    MOE_EHIP = -3,         /* a HIP runtime call failed */
+    MOE_ESTATE = -4,       /* handle destroyed / not usable */
+    MOE_EUNSUPPORTED = -5  /* shape or option outside what the kernels take */
+} moe_status;
+
+/* Per-expert precision tag: the expert's state in the expert cache. */
+typedef enum {
+    MOE_TAG_FP16 = 0,       /* resident at full precision (cache hit) */
+    MOE_TAG_INT4 = 1,       /* resident as its int4 copy: always int4 */
+    MOE_TAG_INT2 = 2,       /* resident as its int2 copy: always int2 */
+    MOE_TAG_MISS_INT4 = 3,  /* cache miss, low copy int4: Eq. 2 rule decides */
+    MOE_TAG_MISS_INT2 = 4   /* cache miss, low copy int2: Eq. 2 rule decides */
+} moe_tag;
+
+/* Precision class used for one (token, slot), as reported in prec_used. */
+enum { MOE_PREC_HIGH = 0, MOE_PREC_LOW = 1, MOE_PREC_SKIP = 2 };
+
+/* Layer shape and rule parameters.
+ *  d_model, d_ff  multiples of 32 (the quantisation group), d_model <= 16384,
+ *                 d_ff <= 65536
+ *  n_experts      1..64;  top_k 1..min(8, n_experts)
+ *  group_size     must be 32
+ *  max_tokens     largest n_tokens any call will pass (sizes the workspace);
+ *                 1..8192
+ *  t1, t2         Eq. 2 thresholds (Section 3.2); t2 >= 1 disables skipping
+ *  rms_eps        epsilon of the RMSNorm used by the *_residual entry points
+ *  flags          reserved, must be 0 */
+typedef struct {
+    int32_t d_model;
+    int32_t d_ff;
+    int32_t n_experts;
+    int32_t top_k;
+    int32_t group_size;
+    int32_t max_tokens;
+    float t1;
+    float t2;
+    float rms_eps;
+    uint32_t flags;
+} moe_layer_desc;
+
+/* Create a layer.  Eq. 1 gating and experts.
+ *  w_router  device, fp16 [n_experts, d_model], borrowed
+ *  w1, w3    host arrays of n_experts device pointers, fp16 [d_ff, d_model]
+ *  w2        host array of n_experts device pointers, fp16 [d_model, d_ff]
+ * The fp16 weights are borrowed: they must stay valid and unchanged for the
+ * life of the handle.  The pointer arrays themselves are copied.  Every
+ * expert starts tagged MOE_TAG_FP16.  Allocates the workspace and the
+ * device expert table; synchronises `stream`.  *out receives the handle. */
+moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
+                          const void* const* w1, const void* const* w3,
+                          const void* const* w2, void* stream,
+                          moe_layer_t* out);
+
+/* Set an expert's precision tag (Section 3.2 / 3.4: its cache state).  A tag
+ * that needs a low-precision copy builds it from the fp16 weights with the
+ * quantiser above the first time (allocating it: library-owned, freed by
+ * moe_layer_destroy); the table entry is updated in stream order, so calls
+ * enqueued later on `stream` see the new tag. */
+moe_status moe_set_expert_precision(moe_layer_t layer, int32_t expert,
+                                    int32_t tag, void* stream);
+
+/* One decode step of the layer (Eq. 1 with the Section 3.2 rule), for
+ * 1 <= n_tokens <= min(max_tokens, 64) tokens.
+ *  x          device, fp16 [n_tokens, d_model] (input hidden states)
+ *  y          device, fp32 [n_tokens, d_model] (output, overwritten)
+ *  topk_idx   device int32 [n_tokens, top_k] or NULL: selected experts,
+ *             slot 0 = largest logit (exact ties: lower index first)
+ *  topk_w     device fp32 [n_tokens, top_k] or NULL: normalised gate values
+ *  prec_used  device int8 [n_tokens, top_k] or NULL: MOE_PREC_* per slot */
+moe_status moe_decode_step(moe_layer_t layer, int32_t n_tokens, const void* x,
+                           float* y, int32_t* topk_idx, float* topk_w,
+                           int8_t* prec_used, void* stream);
+
+/* Decode step with the residual glue used between stacked layers:
+ *  h       device fp32 [n_tokens, d_model], in/out: h += MoE(x)
+ *  x_next  device fp16 [n_tokens, d_model], out: fp16(rmsnorm(h)) with
+ *          rmsnorm(v) = v / sqrt(mean(v^2) + rms_eps) (no gain)
+ * Other arguments as moe_decode_step. */
+moe_status moe_decode_step_residual(moe_layer_t layer, int32_t n_tokens,
+                                    const void* x, float* h, void* x_next,
+                                    int32_t* topk_idx, float* topk_w,
+                                    int8_t* prec_used, void* stream);
+
+/* Prefill: the same layer for 1 <= n_tokens <= max_tokens tokens, with the
+ * experts run as an MFMA grouped GEMM.  Arguments as moe_decode_step. */
+moe_status moe_prefill(moe_layer_t layer, int32_t n_tokens, const void* x,
+                       float* y, int32_t* topk_idx, float* topk_w,
+                       int8_t* prec_used, void* stream);
+
+/* Prefill with the residual glue (see moe_decode_step_residual). */
+moe_status moe_prefill_residual(moe_layer_t layer, int32_t n_tokens,
+                                const void* x, float* h, void* x_next,
+                                int32_t* topk_idx, float* topk_w,
+                                int8_t* prec_used, void* stream);
+
+/* Copy an expert's low-precision copy out (for inspection and parity).
+ *  matrix  0 = W1, 1 = W3, 2 = W2;  bits 4 or 2 (the copy must exist)
+ *  codes   device u8 [rows, cols*bits/8];  scales device fp16 [rows, cols/32]
+ * where [rows, cols] is the matrix's shape. */
+moe_status moe_export_packed(moe_layer_t layer, int32_t expert, int32_t matrix,
+                             int32_t bits, void* codes, void* scales,
+                             void* stream);
+
+/* Quantise any fp16 matrix with the layer's quantiser (the format above).
+ *  w       device fp16 [rows, cols]; cols a multiple of 32
+ *  codes   device u8 [rows, cols*bits/8];  scales device fp16 [rows, cols/32]
+ *  bits    4 or 2.  Needs no handle. */
+moe_status moe_quantize(const void* w, int64_t rows, int64_t cols, int32_t bits,
+                        void* codes, void* scales, void* stream);
+
+/* Free the handle, its workspace and its low-precision copies (synchronises
+ * the device first).  The borrowed fp16 weights are not touched. */
+moe_status moe_layer_destroy(moe_layer_t layer);
+
+/* Thread-local text of the last error on this thread ("" if none). */
+const char* moe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

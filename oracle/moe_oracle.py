@@ -247,14 +247,18 @@ class Expert:
     tag: int = TAG_FP16
 
     def weights(self, prec: int):
-        """float64 weights at the requested precision class."""
-        if prec == PREC_HIGH:
-            return (self.w1.astype(np.float64), self.w3.astype(np.float64),
-                    self.w2.astype(np.float64))
-        bits = low_bits_of_tag(self.tag)
-        assert bits in (2, 4), "low precision requested for an fp16-only expert"
-        return tuple(make_low_copy(w, bits).dense()
-                     for w in (self.w1, self.w3, self.w2))
+        """float64 weights at the requested precision class (memoised)."""
+        memo = self.__dict__.setdefault("_memo", {})
+        if prec not in memo:
+            if prec == PREC_HIGH:
+                memo[prec] = (self.w1.astype(np.float64), self.w3.astype(np.float64),
+                              self.w2.astype(np.float64))
+            else:
+                bits = low_bits_of_tag(self.tag)
+                assert bits in (2, 4), "low precision requested for an fp16-only expert"
+                memo[prec] = tuple(make_low_copy(w, bits).dense()
+                                   for w in (self.w1, self.w3, self.w2))
+        return memo[prec]
 
 
 @dataclass
@@ -285,19 +289,16 @@ def route(x16: np.ndarray, wg16: np.ndarray, tags, k: int,
     return Routing(idx, w, prec, l)
 
 
-def layer_forward(x16: np.ndarray, wg16: np.ndarray, experts, k: int,
-                  t1: float, t2: float, forced_idx=None):
-    """Eq. 1: y[t] = sum_k w[t,k] * E_{idx[t,k]}(x[t]) with each expert at the
-    precision Section 3.2 chose; a skipped term is zero.  Returns (y, routing)
-    with y float64 [T, d]."""
-    tags = [e.tag for e in experts]
-    r = route(x16, wg16, tags, k, t1, t2, forced_idx)
+def layer_output(x16: np.ndarray, experts, r: Routing) -> np.ndarray:
+    """Eq. 1 for given routing decisions: y[t] = sum_k w[t,k] * E_{idx[t,k]}(x[t])
+    with each expert at the precision class r.prec chose; a skipped term is
+    zero.  ``experts[e]`` yields an Expert (it may be built on demand)."""
     x = np.asarray(x16, dtype=np.float64)
     T, d = x.shape
     y = np.zeros((T, d), dtype=np.float64)
     cache = {}
     for t in range(T):
-        for j in range(k):
+        for j in range(r.idx.shape[1]):
             p = int(r.prec[t, j])
             if p == PREC_SKIP:
                 continue
@@ -306,7 +307,16 @@ def layer_forward(x16: np.ndarray, wg16: np.ndarray, experts, k: int,
                 cache[(e, p)] = experts[e].weights(p)
             w1, w3, w2 = cache[(e, p)]
             y[t] += r.w[t, j] * swiglu_expert(x[t:t + 1], w1, w3, w2)[0]
-    return y, r
+    return y
+
+
+def layer_forward(x16: np.ndarray, wg16: np.ndarray, experts, k: int,
+                  t1: float, t2: float, forced_idx=None):
+    """Eq. 1 with the Section 3.2 decisions: route, then layer_output.
+    Returns (y, routing) with y float64 [T, d]."""
+    tags = [e.tag for e in experts]
+    r = route(x16, wg16, tags, k, t1, t2, forced_idx)
+    return layer_output(x16, experts, r), r
 
 
 # --------------------------------------------------------------------------

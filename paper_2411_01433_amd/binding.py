@@ -1,0 +1,205 @@
+"""Thin ctypes binding of the C ABI in include/moe.h.
+
+Argument marshalling only: torch tensors are checked (device, dtype, shape,
+contiguity, alignment) and their data pointers are passed to the library;
+every step of the layer runs in the HIP kernels of libmoe.so.  There is no
+fallback: if the library is missing, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmoe.so")
+
+MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+TAG_FP16, TAG_INT4, TAG_INT2, TAG_MISS_INT4, TAG_MISS_INT2 = 0, 1, 2, 3, 4
+PREC_HIGH, PREC_LOW, PREC_SKIP = 0, 1, 2
+
+EXPORTED = (
+    "moe_layer_init", "moe_set_expert_precision", "moe_decode_step",
+    "moe_decode_step_residual", "moe_prefill", "moe_prefill_residual",
+    "moe_export_packed", "moe_quantize", "moe_layer_destroy", "moe_last_error",
+)
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"moe status {status}: {msg}")
+        self.status = status
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [
+        ("d_model", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+        ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+        ("group_size", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
+        ("t1", ctypes.c_float), ("t2", ctypes.c_float),
+        ("rms_eps", ctypes.c_float), ("flags", ctypes.c_uint32),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmoe.so (built by paper_2411_01433_amd.build); raise if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: run python -m paper_2411_01433_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32p = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+    L.moe_layer_init.argtypes = [ctypes.POINTER(LayerDesc), vp, ctypes.POINTER(vp),
+                                 ctypes.POINTER(vp), ctypes.POINTER(vp), vp,
+                                 ctypes.POINTER(vp)]
+    L.moe_set_expert_precision.argtypes = [vp, i32, i32, vp]
+    step = [vp, i32, vp, f32p, vp, vp, vp, vp]
+    L.moe_decode_step.argtypes = step
+    L.moe_prefill.argtypes = step
+    res = [vp, i32, vp, f32p, vp, vp, vp, vp, vp]
+    L.moe_decode_step_residual.argtypes = res
+    L.moe_prefill_residual.argtypes = res
+    L.moe_export_packed.argtypes = [vp, i32, i32, i32, vp, vp, vp]
+    L.moe_quantize.argtypes = [vp, i64, i64, i32, vp, vp, vp]
+    L.moe_layer_destroy.argtypes = [vp]
+    L.moe_last_error.restype = ctypes.c_char_p
+    for name in EXPORTED:
+        if name != "moe_last_error":
+            getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != MOE_OK:
+        raise MoeError(status, lib().moe_last_error().decode())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _ptr(t, dtype, shape=None, name="tensor"):
+    import torch
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def quantize(w, bits: int, codes, scales, stream=None):
+    """Quantise an fp16 device matrix w [rows, cols] into codes / scales."""
+    import torch
+    rows, cols = w.shape
+    _check(lib().moe_quantize(
+        _ptr(w, torch.float16, None, "w"), rows, cols, bits,
+        _ptr(codes, torch.uint8, (rows, cols * bits // 8), "codes"),
+        _ptr(scales, torch.float16, (rows, cols // 32), "scales"), _stream(stream)))
+
+
+class MoeLayer:
+    """One MoE layer handle over borrowed fp16 device weights.
+
+    w_router [E, d]; w1, w3: lists of E tensors [f, d]; w2: list of E [d, f].
+    The tensors must outlive the layer (the library borrows them).
+    """
+
+    def __init__(self, d_model, d_ff, n_experts, top_k, max_tokens, w_router,
+                 w1, w3, w2, t1=1.0, t2=1.0, rms_eps=1e-5, stream=None):
+        import torch
+        self.d, self.f, self.E, self.K = d_model, d_ff, n_experts, top_k
+        self.max_tokens = max_tokens
+        self._keep = (w_router, list(w1), list(w3), list(w2))
+        desc = LayerDesc(d_model, d_ff, n_experts, top_k, 32, max_tokens,
+                         t1, t2, rms_eps, 0)
+        E = n_experts
+        if not (len(w1) == len(w3) == len(w2) == E):
+            raise ValueError("need one W1, W3 and W2 per expert")
+        arr = ctypes.c_void_p * E
+        p1 = arr(*[_ptr(w, torch.float16, (d_ff, d_model), "w1").value for w in w1])
+        p3 = arr(*[_ptr(w, torch.float16, (d_ff, d_model), "w3").value for w in w3])
+        p2 = arr(*[_ptr(w, torch.float16, (d_model, d_ff), "w2").value for w in w2])
+        h = ctypes.c_void_p()
+        _check(lib().moe_layer_init(ctypes.byref(desc),
+                                    _ptr(w_router, torch.float16, (E, d_model), "w_router"),
+                                    p1, p3, p2, _stream(stream), ctypes.byref(h)))
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def set_expert_precision(self, expert: int, tag: int, stream=None):
+        _check(lib().moe_set_expert_precision(self._h, expert, tag, _stream(stream)))
+
+    def _outs(self, T, topk_idx, topk_w, prec_used):
+        import torch
+        return (_ptr(topk_idx, torch.int32, (T, self.K), "topk_idx"),
+                _ptr(topk_w, torch.float32, (T, self.K), "topk_w"),
+                _ptr(prec_used, torch.int8, (T, self.K), "prec_used"))
+
+    def _step(self, fn, x, y, topk_idx, topk_w, prec_used, stream):
+        import torch
+        T = x.shape[0]
+        _check(fn(self._h, T, _ptr(x, torch.float16, (T, self.d), "x"),
+                  _ptr(y, torch.float32, (T, self.d), "y"),
+                  *self._outs(T, topk_idx, topk_w, prec_used), _stream(stream)))
+
+    def _step_res(self, fn, x, h, x_next, topk_idx, topk_w, prec_used, stream):
+        import torch
+        T = x.shape[0]
+        _check(fn(self._h, T, _ptr(x, torch.float16, (T, self.d), "x"),
+                  _ptr(h, torch.float32, (T, self.d), "h"),
+                  _ptr(x_next, torch.float16, (T, self.d), "x_next"),
+                  *self._outs(T, topk_idx, topk_w, prec_used), _stream(stream)))
+
+    def decode_step(self, x, y, topk_idx=None, topk_w=None, prec_used=None, stream=None):
+        self._step(lib().moe_decode_step, x, y, topk_idx, topk_w, prec_used, stream)
+
+    def prefill(self, x, y, topk_idx=None, topk_w=None, prec_used=None, stream=None):
+        self._step(lib().moe_prefill, x, y, topk_idx, topk_w, prec_used, stream)
+
+    def decode_step_residual(self, x, h, x_next, topk_idx=None, topk_w=None,
+                             prec_used=None, stream=None):
+        self._step_res(lib().moe_decode_step_residual, x, h, x_next, topk_idx,
+                       topk_w, prec_used, stream)
+
+    def prefill_residual(self, x, h, x_next, topk_idx=None, topk_w=None,
+                         prec_used=None, stream=None):
+        self._step_res(lib().moe_prefill_residual, x, h, x_next, topk_idx,
+                       topk_w, prec_used, stream)
+
+    def export_packed(self, expert: int, matrix: int, bits: int, codes, scales,
+                      stream=None):
+        import torch
+        rows, cols = (self.f, self.d) if matrix < 2 else (self.d, self.f)
+        _check(lib().moe_export_packed(
+            self._h, expert, matrix, bits,
+            _ptr(codes, torch.uint8, (rows, cols * bits // 8), "codes"),
+            _ptr(scales, torch.float16, (rows, cols // 32), "scales"), _stream(stream)))
+
+    def destroy(self):
+        if self._h is not None and self._h.value:
+            _check(lib().moe_layer_destroy(self._h))
+        self._h = None
+        self._keep = None
+
+    def __del__(self):
+        try:
+            if getattr(self, "_h", None) is not None and self._h.value:
+                lib().moe_layer_destroy(self._h)
+        except Exception:
+            pass

@@ -1,0 +1,422 @@
+// Host runtime behind include/moe.h: argument validation, handle registry,
+// workspace, expert table and the launch sequence of one layer call.
+#include "../../include/moe.h"
+
+#include <hip/hip_runtime.h>
+
+#include <array>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "moe_internal.h"
+
+using namespace moe;
+
+namespace {
+
+thread_local std::string g_err;
+
+moe_status fail(moe_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+moe_status hip_fail(hipError_t e, const char* what) {
+  return fail(MOE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                    \
+  do {                                         \
+    hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+struct moe_layer {
+  moe_layer_desc desc;
+  int device = -1;
+  const f16* w_router = nullptr;
+  std::vector<ExpertEntry> host_table;
+  // library-owned low-precision copies: [expert][bits==4 ? 0 : 1][matrix]
+  std::vector<void*> owned;
+  std::vector<std::array<std::array<uint8_t*, 3>, 2>> low_q;
+  std::vector<std::array<std::array<f16*, 3>, 2>> low_s;
+  // device memory
+  ExpertEntry* d_table = nullptr;
+  WorkList* d_wl = nullptr;
+  int32_t* d_perm = nullptr;
+  int32_t* d_pos = nullptr;
+  int32_t* d_idx = nullptr;
+  float* d_w = nullptr;
+  int8_t* d_prec = nullptr;
+  f16* d_h = nullptr;       // [max_tokens*K, f]
+  float* d_part = nullptr;  // decode: [n_split, min(max_tokens,64)*K, d]
+  f16* d_xperm = nullptr;   // prefill: [max_tokens*K, d]
+  float* d_eperm = nullptr; // prefill: [max_tokens*K, d]
+  void* arena = nullptr;
+};
+
+namespace {
+
+std::mutex g_mu;
+std::set<moe_layer*> g_live;
+
+bool live(moe_layer* l) {
+  std::lock_guard<std::mutex> g(g_mu);
+  return g_live.count(l) != 0;
+}
+
+moe_status check_desc(const moe_layer_desc* d) {
+  if (!d) return fail(MOE_EINVAL, "desc is NULL");
+  if (d->group_size != kGroup) return fail(MOE_EINVAL, "group_size must be 32 (got %d)", d->group_size);
+  if (d->d_model <= 0 || d->d_model % 64 || d->d_model > 16384)
+    return fail(MOE_EINVAL, "d_model must be a positive multiple of 64, <= 16384 (got %d)", d->d_model);
+  if (d->d_ff <= 0 || d->d_ff % 64 || d->d_ff > 65536)
+    return fail(MOE_EINVAL, "d_ff must be a positive multiple of 64, <= 65536 (got %d)", d->d_ff);
+  if (d->n_experts < 1 || d->n_experts > kMaxExperts)
+    return fail(MOE_EINVAL, "n_experts must be in [1, 64] (got %d)", d->n_experts);
+  if (d->top_k < 1 || d->top_k > kMaxTopK || d->top_k > d->n_experts)
+    return fail(MOE_EINVAL, "top_k must be in [1, min(8, n_experts)] (got %d)", d->top_k);
+  if (d->max_tokens < 1 || d->max_tokens > 8192)
+    return fail(MOE_EINVAL, "max_tokens must be in [1, 8192] (got %d)", d->max_tokens);
+  if (!(d->t1 == d->t1) || !(d->t2 == d->t2) || !(d->rms_eps >= 0.0f))
+    return fail(MOE_EINVAL, "t1, t2 must be numbers and rms_eps >= 0");
+  if (d->flags != 0) return fail(MOE_EINVAL, "flags must be 0");
+  return MOE_OK;
+}
+
+int n_split_of(int f) { return (f + kSplitCols - 1) / kSplitCols; }
+
+moe_status check_call(moe_layer* l, int32_t n_tokens, int32_t limit,
+                      const void* x, const void* out0, const void* out1) {
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  if (n_tokens < 1 || n_tokens > limit)
+    return fail(MOE_EINVAL, "n_tokens must be in [1, %d] (got %d)", limit, n_tokens);
+  if (!x || !out0) return fail(MOE_EINVAL, "x and the output must not be NULL");
+  if (!aligned16(x) || !aligned16(out0) || (out1 && !aligned16(out1)))
+    return fail(MOE_EINVAL, "x and outputs must be 16-byte aligned");
+  return MOE_OK;
+}
+
+moe_status set_device(moe_layer* l) {
+  HIP_TRY(hipSetDevice(l->device), "hipSetDevice");
+  return MOE_OK;
+}
+
+RouteParams route_params(moe_layer* l, int T, const void* x) {
+  RouteParams p;
+  p.x = static_cast<const f16*>(x);
+  p.wg = l->w_router;
+  p.table = l->d_table;
+  p.T = T;
+  p.d = l->desc.d_model;
+  p.E = l->desc.n_experts;
+  p.K = l->desc.top_k;
+  p.t1 = l->desc.t1;
+  p.t2 = l->desc.t2;
+  return p;
+}
+
+RouteOut route_out(moe_layer* l, int32_t* idx, float* w, int8_t* prec) {
+  RouteOut o;
+  o.idx = l->d_idx;
+  o.w = l->d_w;
+  o.prec = l->d_prec;
+  o.user_idx = idx;
+  o.user_w = w;
+  o.user_prec = prec;
+  return o;
+}
+
+int max_groups_of(moe_layer* l, int T) {
+  const int a = T * l->desc.top_k, b = 2 * l->desc.n_experts;
+  return a < b ? a : b;
+}
+
+moe_status decode_impl(moe_layer* l, int32_t T, const void* x, float* y,
+                       float* h_res, void* x_next, int32_t* idx, float* w,
+                       int8_t* prec, void* stream) {
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  const int lim = l->desc.max_tokens < kDecodeMaxTokens ? l->desc.max_tokens : kDecodeMaxTokens;
+  moe_status st = check_call(l, T, lim, x, h_res ? (const void*)h_res : (const void*)y, x_next);
+  if (st != MOE_OK) return st;
+  if (h_res && !x_next) return fail(MOE_EINVAL, "x_next must not be NULL");
+  if ((st = set_device(l)) != MOE_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
+  const int mg = max_groups_of(l, T);
+  HIP_TRY(launch_route_decode(route_params(l, T, x), route_out(l, idx, w, prec),
+                              l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
+  HIP_TRY(launch_decode_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
+                           l->d_h, T, d, f, K, mg, s), "up kernel launch");
+  HIP_TRY(launch_decode_down(l->d_table, l->d_wl, l->d_perm, l->d_h, l->d_part, T,
+                             d, f, K, mg, s), "down kernel launch");
+  HIP_TRY(launch_combine_decode(l->d_part, l->d_w, l->d_prec, n_split_of(f), T, d, K,
+                                y, h_res, static_cast<f16*>(x_next),
+                                l->desc.rms_eps, s), "combine kernel launch");
+  return MOE_OK;
+}
+
+moe_status prefill_impl(moe_layer* l, int32_t T, const void* x, float* y,
+                        float* h_res, void* x_next, int32_t* idx, float* w,
+                        int8_t* prec, void* stream) {
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  moe_status st = check_call(l, T, l->desc.max_tokens, x,
+                             h_res ? (const void*)h_res : (const void*)y, x_next);
+  if (st != MOE_OK) return st;
+  if (h_res && !x_next) return fail(MOE_EINVAL, "x_next must not be NULL");
+  if ((st = set_device(l)) != MOE_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
+  const int mg = max_groups_of(l, T);
+  HIP_TRY(launch_route_prefill(route_params(l, T, x), route_out(l, idx, w, prec),
+                               l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
+  HIP_TRY(launch_prefill_experts(l->d_table, l->d_wl, l->d_perm,
+                                 static_cast<const f16*>(x), l->d_xperm, l->d_h,
+                                 l->d_eperm, T, d, f, K, mg, s), "prefill expert launch");
+  HIP_TRY(launch_combine_prefill(l->d_eperm, l->d_pos, l->d_w, l->d_prec, T, d, K, y,
+                                 h_res, static_cast<f16*>(x_next), l->desc.rms_eps, s),
+          "combine kernel launch");
+  return MOE_OK;
+}
+
+void free_layer(moe_layer* l) {
+  for (void* p : l->owned) (void)hipFree(p);
+  if (l->arena) (void)hipFree(l->arena);
+  delete l;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* moe_last_error(void) { return g_err.c_str(); }
+
+moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
+                          const void* const* w1, const void* const* w3,
+                          const void* const* w2, void* stream, moe_layer_t* out) {
+  g_err.clear();
+  if (!out) return fail(MOE_EINVAL, "out is NULL");
+  *out = nullptr;
+  moe_status st = check_desc(desc);
+  if (st != MOE_OK) return st;
+  if (!w_router || !w1 || !w3 || !w2) return fail(MOE_EINVAL, "weight pointers must not be NULL");
+  if (!aligned16(w_router)) return fail(MOE_EINVAL, "w_router must be 16-byte aligned");
+  for (int e = 0; e < desc->n_experts; ++e) {
+    if (!w1[e] || !w3[e] || !w2[e]) return fail(MOE_EINVAL, "expert %d has a NULL weight pointer", e);
+    if (!aligned16(w1[e]) || !aligned16(w3[e]) || !aligned16(w2[e]))
+      return fail(MOE_EINVAL, "expert %d weights must be 16-byte aligned", e);
+  }
+  moe_layer* l = new (std::nothrow) moe_layer();
+  if (!l) return fail(MOE_ENOMEM, "host allocation failed");
+  l->desc = *desc;
+  hipError_t he = hipGetDevice(&l->device);
+  if (he != hipSuccess) { delete l; return hip_fail(he, "hipGetDevice"); }
+  l->w_router = static_cast<const f16*>(w_router);
+  const int E = desc->n_experts, K = desc->top_k, d = desc->d_model, f = desc->d_ff;
+  const int64_t M = desc->max_tokens;
+  const int64_t Md = M < kDecodeMaxTokens ? M : kDecodeMaxTokens;
+  l->host_table.resize(E);
+  l->low_q.resize(E);
+  l->low_s.resize(E);
+  for (int e = 0; e < E; ++e) {
+    ExpertEntry& x = l->host_table[e];
+    std::memset(&x, 0, sizeof x);
+    x.w[0] = static_cast<const f16*>(w1[e]);
+    x.w[1] = static_cast<const f16*>(w3[e]);
+    x.w[2] = static_cast<const f16*>(w2[e]);
+    x.tag = TAG_FP16;
+    for (auto& a : l->low_q[e]) a.fill(nullptr);
+    for (auto& a : l->low_s[e]) a.fill(nullptr);
+  }
+  // one arena: every region 256-byte aligned
+  auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  size_t off = 0;
+  const size_t o_table = off; off += al(sizeof(ExpertEntry) * E);
+  const size_t o_wl = off;    off += al(sizeof(WorkList));
+  const size_t o_perm = off;  off += al(sizeof(int32_t) * M * K);
+  const size_t o_pos = off;   off += al(sizeof(int32_t) * M * K);
+  const size_t o_idx = off;   off += al(sizeof(int32_t) * M * K);
+  const size_t o_w = off;     off += al(sizeof(float) * M * K);
+  const size_t o_prec = off;  off += al(sizeof(int8_t) * M * K);
+  const size_t o_h = off;     off += al(sizeof(f16) * M * K * f);
+  const size_t o_part = off;  off += al(sizeof(float) * n_split_of(f) * Md * K * d);
+  const size_t o_xp = off;    off += al(sizeof(f16) * M * K * d);
+  const size_t o_ep = off;    off += al(sizeof(float) * M * K * d);
+  he = hipMalloc(&l->arena, off);
+  if (he != hipSuccess) {
+    delete l;
+    return fail(MOE_ENOMEM, "hipMalloc of %zu workspace bytes failed: %s", off, hipGetErrorString(he));
+  }
+  char* base = static_cast<char*>(l->arena);
+  l->d_table = reinterpret_cast<ExpertEntry*>(base + o_table);
+  l->d_wl = reinterpret_cast<WorkList*>(base + o_wl);
+  l->d_perm = reinterpret_cast<int32_t*>(base + o_perm);
+  l->d_pos = reinterpret_cast<int32_t*>(base + o_pos);
+  l->d_idx = reinterpret_cast<int32_t*>(base + o_idx);
+  l->d_w = reinterpret_cast<float*>(base + o_w);
+  l->d_prec = reinterpret_cast<int8_t*>(base + o_prec);
+  l->d_h = reinterpret_cast<f16*>(base + o_h);
+  l->d_part = reinterpret_cast<float*>(base + o_part);
+  l->d_xperm = reinterpret_cast<f16*>(base + o_xp);
+  l->d_eperm = reinterpret_cast<float*>(base + o_ep);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  he = hipMemcpyAsync(l->d_table, l->host_table.data(), sizeof(ExpertEntry) * E,
+                      hipMemcpyHostToDevice, s);
+  if (he == hipSuccess) he = hipMemsetAsync(l->d_wl, 0, sizeof(WorkList), s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
+  if (he != hipSuccess) {
+    free_layer(l);
+    return hip_fail(he, "layer init copy");
+  }
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    g_live.insert(l);
+  }
+  *out = l;
+  return MOE_OK;
+}
+
+moe_status moe_set_expert_precision(moe_layer_t l, int32_t expert, int32_t tag,
+                                    void* stream) {
+  g_err.clear();
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  if (expert < 0 || expert >= l->desc.n_experts)
+    return fail(MOE_EINVAL, "expert %d out of range [0, %d)", expert, l->desc.n_experts);
+  if (tag < MOE_TAG_FP16 || tag > MOE_TAG_MISS_INT2) return fail(MOE_EINVAL, "unknown tag %d", tag);
+  moe_status st = set_device(l);
+  if (st != MOE_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ExpertEntry v = l->host_table[expert];
+  v.tag = tag;
+  const int bits = (tag == MOE_TAG_INT4 || tag == MOE_TAG_MISS_INT4) ? 4
+                   : (tag == MOE_TAG_INT2 || tag == MOE_TAG_MISS_INT2) ? 2 : 0;
+  if (bits) {
+    const int slot = bits == 4 ? 0 : 1;
+    const int d = l->desc.d_model, f = l->desc.d_ff;
+    for (int m = 0; m < 3; ++m) {
+      const int64_t rows = m < 2 ? f : d, cols = m < 2 ? d : f;
+      if (!l->low_q[expert][slot][m]) {
+        void *q = nullptr, *sc = nullptr;
+        hipError_t he = hipMalloc(&q, (size_t)rows * cols * bits / 8);
+        if (he == hipSuccess) he = hipMalloc(&sc, (size_t)rows * (cols / kGroup) * sizeof(f16));
+        if (he != hipSuccess) {
+          if (q) (void)hipFree(q);
+          return fail(MOE_ENOMEM, "allocation of the int%d copy failed: %s", bits, hipGetErrorString(he));
+        }
+        l->owned.push_back(q);
+        l->owned.push_back(sc);
+        l->low_q[expert][slot][m] = static_cast<uint8_t*>(q);
+        l->low_s[expert][slot][m] = static_cast<f16*>(sc);
+        HIP_TRY(launch_quantize(v.w[m], rows, cols, bits, static_cast<uint8_t*>(q),
+                                static_cast<f16*>(sc), s), "quantize kernel launch");
+      }
+      v.q[m] = l->low_q[expert][slot][m];
+      v.s[m] = l->low_s[expert][slot][m];
+    }
+    v.low_bits = bits;
+  } else {
+    for (int m = 0; m < 3; ++m) { v.q[m] = nullptr; v.s[m] = nullptr; }
+    v.low_bits = 0;
+  }
+  l->host_table[expert] = v;
+  HIP_TRY(launch_set_entry(l->d_table, expert, v, s), "table update launch");
+  return MOE_OK;
+}
+
+moe_status moe_decode_step(moe_layer_t l, int32_t n_tokens, const void* x, float* y,
+                           int32_t* topk_idx, float* topk_w, int8_t* prec_used,
+                           void* stream) {
+  g_err.clear();
+  return decode_impl(l, n_tokens, x, y, nullptr, nullptr, topk_idx, topk_w, prec_used, stream);
+}
+
+moe_status moe_decode_step_residual(moe_layer_t l, int32_t n_tokens, const void* x,
+                                    float* h, void* x_next, int32_t* topk_idx,
+                                    float* topk_w, int8_t* prec_used, void* stream) {
+  g_err.clear();
+  return decode_impl(l, n_tokens, x, nullptr, h, x_next, topk_idx, topk_w, prec_used, stream);
+}
+
+moe_status moe_prefill(moe_layer_t l, int32_t n_tokens, const void* x, float* y,
+                       int32_t* topk_idx, float* topk_w, int8_t* prec_used, void* stream) {
+  g_err.clear();
+  return prefill_impl(l, n_tokens, x, y, nullptr, nullptr, topk_idx, topk_w, prec_used, stream);
+}
+
+moe_status moe_prefill_residual(moe_layer_t l, int32_t n_tokens, const void* x, float* h,
+                                void* x_next, int32_t* topk_idx, float* topk_w,
+                                int8_t* prec_used, void* stream) {
+  g_err.clear();
+  return prefill_impl(l, n_tokens, x, nullptr, h, x_next, topk_idx, topk_w, prec_used, stream);
+}
+
+moe_status moe_export_packed(moe_layer_t l, int32_t expert, int32_t matrix, int32_t bits,
+                             void* codes, void* scales, void* stream) {
+  g_err.clear();
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  if (expert < 0 || expert >= l->desc.n_experts) return fail(MOE_EINVAL, "expert out of range");
+  if (matrix < 0 || matrix > 2) return fail(MOE_EINVAL, "matrix must be 0, 1 or 2");
+  if (bits != 4 && bits != 2) return fail(MOE_EINVAL, "bits must be 4 or 2");
+  if (!codes || !scales) return fail(MOE_EINVAL, "codes and scales must not be NULL");
+  const int slot = bits == 4 ? 0 : 1;
+  const uint8_t* q = l->low_q[expert][slot][matrix];
+  const f16* sc = l->low_s[expert][slot][matrix];
+  if (!q) return fail(MOE_ESTATE, "expert %d has no int%d copy", expert, bits);
+  moe_status st = set_device(l);
+  if (st != MOE_OK) return st;
+  const int d = l->desc.d_model, f = l->desc.d_ff;
+  const int64_t rows = matrix < 2 ? f : d, cols = matrix < 2 ? d : f;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(hipMemcpyAsync(codes, q, (size_t)rows * cols * bits / 8, hipMemcpyDeviceToDevice, s),
+          "export codes");
+  HIP_TRY(hipMemcpyAsync(scales, sc, (size_t)rows * (cols / kGroup) * sizeof(f16),
+                         hipMemcpyDeviceToDevice, s), "export scales");
+  return MOE_OK;
+}
+
+moe_status moe_quantize(const void* w, int64_t rows, int64_t cols, int32_t bits,
+                        void* codes, void* scales, void* stream) {
+  g_err.clear();
+  if (!w || !codes || !scales) return fail(MOE_EINVAL, "pointers must not be NULL");
+  if (rows < 0 || cols < 0 || cols % kGroup) return fail(MOE_EINVAL, "cols must be a multiple of 32");
+  if (bits != 4 && bits != 2) return fail(MOE_EINVAL, "bits must be 4 or 2");
+  if (rows > 0 && cols / kGroup > (((int64_t)1 << 38) / rows)) return fail(MOE_EINVAL, "matrix too large");
+  if (!aligned16(w) || ((uintptr_t)codes & 7u) || ((uintptr_t)scales & 1u))
+    return fail(MOE_EINVAL, "w must be 16-byte aligned, codes 8-byte, scales 2-byte");
+  if (bits == 4 && ((uintptr_t)codes & 15u)) return fail(MOE_EINVAL, "int4 codes must be 16-byte aligned");
+  HIP_TRY(launch_quantize(static_cast<const f16*>(w), rows, cols, bits,
+                          static_cast<uint8_t*>(codes), static_cast<f16*>(scales),
+                          static_cast<hipStream_t>(stream)), "quantize kernel launch");
+  return MOE_OK;
+}
+
+moe_status moe_layer_destroy(moe_layer_t l) {
+  g_err.clear();
+  if (!l) return fail(MOE_EINVAL, "layer is NULL");
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    if (!g_live.erase(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  }
+  hipError_t he = hipSetDevice(l->device);
+  if (he == hipSuccess) he = hipDeviceSynchronize();
+  free_layer(l);
+  if (he != hipSuccess) return hip_fail(he, "destroy synchronize");
+  return MOE_OK;
+}
+
+}  // extern "C"

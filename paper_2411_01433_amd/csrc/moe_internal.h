@@ -1,0 +1,105 @@
+// Internal types shared by the HIP kernels and the host runtime of the
+// mixed-precision MoE layer.  Not part of the public ABI (include/moe.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef _Float16 f16;
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGroup = 32;          // quantisation group along the input dim
+constexpr int kMaxExperts = 64;
+constexpr int kMaxTopK = 8;
+constexpr int kMaxKeys = 2 * kMaxExperts;  // (expert, high|low) work groups
+constexpr int kDecodeMaxTokens = 64;
+constexpr int kSplitCols = 4096;    // K-split width of the decode down-proj
+
+enum { PREC_HIGH = 0, PREC_LOW = 1, PREC_SKIP = 2 };
+enum { TAG_FP16 = 0, TAG_INT4 = 1, TAG_INT2 = 2, TAG_MISS_INT4 = 3,
+       TAG_MISS_INT2 = 4 };
+
+// Device-side expert table entry: where each copy of one expert lives and
+// which cache state (tag) it is in.
+struct ExpertEntry {
+  const f16* w[3];       // fp16 W1, W3 ([f, d]) and W2 ([d, f]); borrowed
+  const uint8_t* q[3];   // packed codes of the low copy (bits = low_bits)
+  const f16* s[3];       // fp16 group scales of the low copy
+  int32_t tag;           // TAG_*
+  int32_t low_bits;      // 4 or 2 when a low copy exists, else 0
+  int32_t pad[2];
+};
+
+// One work group: every (token, slot) pair routed to `expert` at one
+// precision.  Pairs are listed contiguously in perm[offset, offset+count).
+struct Group {
+  int32_t expert;
+  int32_t bits;    // 16 (fp16 copy), 4 or 2
+  int32_t offset;
+  int32_t count;
+};
+
+struct WorkList {
+  int32_t n_groups;
+  int32_t max_count;   // largest group (tokens of the busiest expert copy)
+  int32_t pad[2];
+  Group groups[kMaxKeys];
+};
+
+// Routing outputs of one call; optional user copies may be null.
+struct RouteOut {
+  int32_t* idx;        // [T*K] internal
+  float* w;            // [T*K] internal
+  int8_t* prec;        // [T*K] internal
+  int32_t* user_idx;   // optional
+  float* user_w;       // optional
+  int8_t* user_prec;   // optional
+};
+
+struct RouteParams {
+  const f16* x;         // [T, d]
+  const f16* wg;        // [E, d]
+  const ExpertEntry* table;
+  int32_t T, d, E, K;
+  float t1, t2;
+};
+
+// ---- launchers (defined in the .hip files) -------------------------------
+hipError_t launch_quantize(const f16* w, int64_t rows, int64_t cols, int bits,
+                           uint8_t* codes, f16* scales, hipStream_t s);
+hipError_t launch_set_entry(ExpertEntry* table, int e, ExpertEntry v,
+                            hipStream_t s);
+hipError_t launch_route_decode(const RouteParams& p, RouteOut o, WorkList* wl,
+                               int32_t* perm, int32_t* pos, hipStream_t s);
+hipError_t launch_route_prefill(const RouteParams& p, RouteOut o, WorkList* wl,
+                                int32_t* perm, int32_t* pos, hipStream_t s);
+hipError_t launch_decode_up(const ExpertEntry* table, const WorkList* wl,
+                            const int32_t* perm, const f16* x, f16* h,
+                            int T, int d, int f, int K, int max_groups,
+                            hipStream_t s);
+hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
+                              const int32_t* perm, const f16* h, float* part,
+                              int T, int d, int f, int K, int max_groups,
+                              hipStream_t s);
+hipError_t launch_combine_decode(const float* part, const float* w,
+                                 const int8_t* prec, int n_split, int T, int d,
+                                 int K, float* y, float* h_res, f16* x_next,
+                                 float eps, hipStream_t s);
+hipError_t launch_prefill_experts(const ExpertEntry* table, const WorkList* wl,
+                                  const int32_t* perm, const f16* x,
+                                  f16* x_perm, f16* h_perm, float* e_perm,
+                                  int T, int d, int f, int K, int max_groups,
+                                  hipStream_t s);
+hipError_t launch_combine_prefill(const float* e_perm, const int32_t* pos,
+                                  const float* w, const int8_t* prec, int T,
+                                  int d, int K, float* y, float* h_res,
+                                  f16* x_next, float eps, hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,221 @@
+// Gating and the token-level precision decision.
+//
+//   logits l[t, e] = sum_d x[t, d] Wg[e, d]           (Eq. 1 gate, fp32 acc)
+//   top-k by (l desc, index asc); w = softmax over the K selected logits
+//   (Section 3.2: the gate values are normalised)
+//   Eq. 2: with slots already in descending gate order, s_0 = 0 and
+//   s_j = sum_{i<j} w_i; miss-tagged experts run high if s <= t1, low if
+//   t1 < s <= t2, are skipped if s > t2; slot 0 is always high.
+//
+// Then a work list groups the (token, slot) pairs by (expert, precision):
+// a stable counting sort over pair ids p = t*K + k, so pair order inside a
+// group follows token order and the result is deterministic.
+#include "moe_internal.h"
+
+namespace moe {
+
+namespace {
+
+constexpr int kRouteThreads = 1024;
+constexpr int kPrefillTokPerBlock = 8;
+constexpr int kPrefillThreads = 256;
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Dot products of tokens [t0, t1) against all E gate rows; one wave per
+// (token, expert) pair, 8 fp16 per lane per step.  Results go to lg[t-t0][e].
+__device__ void gate_logits(const RouteParams& p, int t0, int t1, float* lg) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int n_waves = blockDim.x >> 6;
+  const int n_pairs = (t1 - t0) * p.E;
+  for (int q = wave; q < n_pairs; q += n_waves) {
+    const int tl = q / p.E;
+    const int e = q - tl * p.E;
+    const f16* xr = p.x + (int64_t)(t0 + tl) * p.d;
+    const f16* gr = p.wg + (int64_t)e * p.d;
+    float acc = 0.0f;
+    for (int c = lane * 8; c < p.d; c += 64 * 8) {
+      f16x8 a = __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(xr + c));
+      f16x8 b = __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(gr + c));
+#pragma unroll
+      for (int j = 0; j < 8; j += 2)
+        acc = __builtin_amdgcn_fdot2(f16x2{a[j], a[j + 1]},
+                                     f16x2{b[j], b[j + 1]}, acc, false);
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) lg[tl * p.E + e] = acc;
+  }
+}
+
+// top-k, softmax over the selected logits and the Eq. 2 rule for one token.
+__device__ void decide_token(const RouteParams& p, int t, const float* lrow,
+                             RouteOut o) {
+  int sel[kMaxTopK];
+  float ls[kMaxTopK];
+  uint64_t taken = 0;  // E <= 64
+  for (int k = 0; k < p.K; ++k) {
+    int best = -1;
+    float bv = 0.0f;
+    for (int e = 0; e < p.E; ++e) {
+      if (taken >> e & 1ull) continue;
+      const float v = lrow[e];
+      if (best < 0 || v > bv) {  // strict: exact ties keep the lower index
+        best = e;
+        bv = v;
+      }
+    }
+    taken |= 1ull << best;
+    sel[k] = best;
+    ls[k] = bv;
+  }
+  float ex[kMaxTopK];
+  float z = 0.0f;
+  for (int k = 0; k < p.K; ++k) {
+    ex[k] = expf(ls[k] - ls[0]);
+    z += ex[k];
+  }
+  float above = 0.0f;  // Eq. 2 running score
+  for (int k = 0; k < p.K; ++k) {
+    const float w = ex[k] / z;
+    const int e = sel[k];
+    const int tag = p.table[e].tag;
+    int prec;
+    if (tag == TAG_FP16) {
+      prec = PREC_HIGH;
+    } else if (tag == TAG_INT4 || tag == TAG_INT2) {
+      prec = PREC_LOW;
+    } else {
+      const float s = (k == 0) ? 0.0f : above;
+      prec = (k == 0 || s <= p.t1) ? PREC_HIGH
+                                   : (s <= p.t2 ? PREC_LOW : PREC_SKIP);
+    }
+    above += w;
+    const int pi = t * p.K + k;
+    o.idx[pi] = e;
+    o.w[pi] = w;
+    o.prec[pi] = (int8_t)prec;
+    if (o.user_idx) o.user_idx[pi] = e;
+    if (o.user_w) o.user_w[pi] = w;
+    if (o.user_prec) o.user_prec[pi] = (int8_t)prec;
+  }
+}
+
+// Stable counting sort of all T*K pairs by key = expert*2 + (low ? 1 : 0)
+// (skipped pairs get no key).  Run by one whole block.
+__device__ void build_worklist(const RouteParams& p, const int32_t* idx,
+                               const int8_t* prec, WorkList* wl,
+                               int32_t* perm, int32_t* pos) {
+  __shared__ int cnt[kMaxKeys];
+  __shared__ int base[kMaxKeys];
+  __shared__ int chunk_keys[kRouteThreads];
+  const int tid = threadIdx.x;
+  const int N = p.T * p.K;
+  const int n_keys = 2 * p.E;
+  for (int k = tid; k < n_keys; k += blockDim.x) cnt[k] = 0;
+  __syncthreads();
+  for (int i = tid; i < N; i += blockDim.x) {
+    const int pr = prec[i];
+    if (pr != PREC_SKIP) atomicAdd(&cnt[idx[i] * 2 + (pr == PREC_LOW)], 1);
+    else pos[i] = -1;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int off = 0, ng = 0, mx = 0;
+    for (int k = 0; k < n_keys; ++k) {
+      base[k] = off;
+      const int c = cnt[k];
+      if (c > 0) {
+        const int e = k >> 1;
+        Group g;
+        g.expert = e;
+        g.bits = (k & 1) ? p.table[e].low_bits : 16;
+        g.offset = off;
+        g.count = c;
+        wl->groups[ng++] = g;
+        mx = c > mx ? c : mx;
+      }
+      off += c;
+    }
+    wl->n_groups = ng;
+    wl->max_count = mx;
+  }
+  __syncthreads();
+  // placement, one chunk of blockDim pairs at a time
+  for (int c0 = 0; c0 < N; c0 += blockDim.x) {
+    const int i = c0 + tid;
+    int key = -1;
+    if (i < N && prec[i] != PREC_SKIP) key = idx[i] * 2 + (prec[i] == PREC_LOW);
+    chunk_keys[tid] = key;
+    __syncthreads();
+    if (key >= 0) {
+      int r = 0;
+      for (int j = 0; j < tid; ++j) r += (chunk_keys[j] == key);
+      const int at = base[key] + r;
+      perm[at] = i;
+      pos[i] = at;
+    }
+    __syncthreads();
+    // advance bases by this chunk's counts
+    if (tid < n_keys) {
+      int add = 0;
+      const int n_in = min((int)blockDim.x, N - c0);
+      for (int j = 0; j < n_in; ++j) add += (chunk_keys[j] == tid);
+      base[tid] += add;
+    }
+    __syncthreads();
+  }
+}
+
+// Decode: one block routes every token and builds the work list.
+__global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
+    RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
+  __shared__ float lg[kDecodeMaxTokens * kMaxExperts];
+  gate_logits(p, 0, p.T, lg);
+  __syncthreads();
+  for (int t = threadIdx.x; t < p.T; t += blockDim.x)
+    decide_token(p, t, lg + t * p.E, o);
+  __syncthreads();
+  build_worklist(p, o.idx, o.prec, wl, perm, pos);
+}
+
+// Prefill: many blocks route their tokens; a second kernel builds the list.
+__global__ __launch_bounds__(kPrefillThreads) void route_tokens_kernel(
+    RouteParams p, RouteOut o) {
+  __shared__ float lg[kPrefillTokPerBlock * kMaxExperts];
+  const int t0 = blockIdx.x * kPrefillTokPerBlock;
+  const int t1 = min(t0 + kPrefillTokPerBlock, p.T);
+  gate_logits(p, t0, t1, lg);
+  __syncthreads();
+  for (int t = t0 + (int)threadIdx.x; t < t1; t += blockDim.x)
+    decide_token(p, t, lg + (t - t0) * p.E, o);
+}
+
+__global__ __launch_bounds__(kRouteThreads) void worklist_kernel(
+    RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
+  build_worklist(p, o.idx, o.prec, wl, perm, pos);
+}
+
+}  // namespace
+
+hipError_t launch_route_decode(const RouteParams& p, RouteOut o, WorkList* wl,
+                               int32_t* perm, int32_t* pos, hipStream_t s) {
+  route_decode_kernel<<<1, kRouteThreads, 0, s>>>(p, o, wl, perm, pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_route_prefill(const RouteParams& p, RouteOut o, WorkList* wl,
+                                int32_t* perm, int32_t* pos, hipStream_t s) {
+  const int blocks = (p.T + kPrefillTokPerBlock - 1) / kPrefillTokPerBlock;
+  route_tokens_kernel<<<blocks, kPrefillThreads, 0, s>>>(p, o);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  worklist_kernel<<<1, kRouteThreads, 0, s>>>(p, o, wl, perm, pos);
+  return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,265 @@
+"""Parity of the HIP library with the CPU oracle, through the C ABI.
+
+Bar: top-k indices, precision decisions and packed codes bit-exact (near
+ties flagged and resolved as documented in gpu_support.check_routing);
+fp32 outputs within 2e-3 normwise relative error per token row.
+"""
+import numpy as np
+import pytest
+
+from oracle import moe_oracle as O
+from synth import configs as C
+from synth import gen
+
+import gpu_support as S
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2411_01433_amd as P
+    P.lib()  # loud failure if the library was not built
+    yield
+
+
+def _edge(name, seed, d, f, E, K, T, tags, t1=1.0, t2=1.0):
+    return C.Workload(name=name, seed=seed, d_model=d, d_ff=f, n_experts=E,
+                      top_k=K, n_tokens=T, t1=t1, t2=t2, fixed_tags=tuple(tags))
+
+
+def _layer_case(wl, tags, x16, t1=None, t2=None, max_tokens=None, residual=False):
+    """Run one decode step on the device and check it against the oracle."""
+    t1 = wl.t1 if t1 is None else t1
+    t2 = wl.t2 if t2 is None else t2
+    weights = S.device_layer_weights(wl, 0)
+    L = S.make_layer(wl, tags, weights, max_tokens=max_tokens or len(x16), t1=t1, t2=t2)
+    T, d, K = x16.shape[0], wl.d_model, wl.top_k
+    xd = torch.from_numpy(x16).cuda()
+    wg16 = C.router_weight(wl, 0)
+    experts = S.HostExperts(wl, 0, tags)
+    if residual:
+        h0 = np.asarray(x16, dtype=np.float32) * np.float32(0.5)
+        hd = torch.from_numpy(h0).cuda()
+        xn, idx, w, prec = S.run_decode(L, xd, T, d, K, residual_h=hd)
+        h1 = hd.cpu().numpy()
+    else:
+        y, idx, w, prec = S.run_decode(L, xd, T, d, K)
+    r, flags = S.check_routing(x16, wg16, tags, K, t1, t2, idx, w, prec)
+    y_ref = O.layer_output(x16, experts, r)
+    if residual:
+        h_ref, xn_ref = O.residual_step(h0.astype(np.float64), y_ref, O.RMS_EPS)
+        assert S.normwise(h1, h_ref).max() <= S.TOL
+        assert S.normwise(h1 - h0, y_ref).max() <= S.TOL
+        assert S.normwise(xn, O.rmsnorm(h_ref)).max() <= S.TOL
+    else:
+        err = S.normwise(y, y_ref)
+        assert err.max() <= S.TOL, f"normwise error {err.max():.3e}"
+    L.destroy()
+    return r, flags
+
+
+# ------------------------------------------------------------ generator
+def test_generator_matches_host():
+    from synth import gpu as G
+    for (shape, start, std) in (((1000,), 0, 0.02), ((37, 64), 3, 1.0), ((4096,), 517, 0.02)):
+        key = gen.tensor_key(9, 2, gen.TENSOR_W1, 5)
+        t = torch.empty(shape, dtype=torch.float16, device="cuda")
+        G.normal_fp16_(t, key, std, start=start)
+        ref = gen.normal_table(std)[gen.uniform_u16(key, int(np.prod(shape)), start)]
+        assert np.array_equal(t.cpu().numpy().view(np.uint16).ravel(), ref.view(np.uint16))
+
+
+# ------------------------------------------------------------ quantiser
+def _quant_device(w16, bits):
+    import paper_2411_01433_amd as P
+    rows, cols = w16.shape
+    wd = torch.from_numpy(np.ascontiguousarray(w16)).cuda()
+    codes = torch.empty((rows, cols * bits // 8), dtype=torch.uint8, device="cuda")
+    scales = torch.empty((rows, cols // 32), dtype=torch.float16, device="cuda")
+    P.quantize(wd, bits, codes, scales)
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), scales.cpu().numpy()
+
+
+def _quant_cases():
+    rng = np.random.default_rng(7)
+    cases = [(rng.standard_normal((256, 4096)) * 0.02).astype(np.float16),
+             (rng.standard_normal((8, 8192)) * 1e-5).astype(np.float16),   # subnormal scales
+             (rng.standard_normal((3, 96)) * 300).astype(np.float16)]
+    special = np.zeros((6, 64), dtype=np.float16)
+    special[1, :] = np.float16(65504)
+    special[1, 1::2] = np.float16(-65504)
+    special[2, :32] = (np.arange(32) - 16).astype(np.float16) * np.float16(2.0 ** -6) / 2
+    special[3, :] = np.float16(2.0 ** -24)                 # smallest subnormal
+    special[4, :32] = np.float16(-1.0)
+    special[5, 5] = np.float16(7 * 2.0 ** -6)
+    special[5, 6:32] = (np.arange(26) % 15 - 7).astype(np.float16) * np.float16(2.0 ** -7)
+    cases.append(special)
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                    "quant_worked_examples.json")))
+    for c in g["cases"]:
+        cases.append((np.array(c["w_over_2m6"]) * 2.0 ** -6).astype(np.float16)[None, :])
+    return cases
+
+
+@pytest.mark.parametrize("bits", [4, 2])
+def test_quantize_bit_exact(bits):
+    for w in _quant_cases():
+        if w.shape[1] % 32:
+            continue
+        codes, scales = _quant_device(w, bits)
+        q, s = O.quantize(w, bits)
+        assert np.array_equal(scales.view(np.uint16), s.view(np.uint16)), w.shape
+        assert np.array_equal(codes, O.pack_codes(q, bits)), w.shape
+
+
+def test_export_packed_matches_quantizer():
+    wl = C.TINY
+    tags = C.layer_tags(wl, 0)
+    weights = S.device_layer_weights(wl, 0)
+    L = S.make_layer(wl, tags, weights)
+    for e, tag in enumerate(tags):
+        bits = O.low_bits_of_tag(int(tag))
+        if not bits:
+            continue
+        for m, (rows, cols) in enumerate([(wl.d_ff, wl.d_model)] * 2 + [(wl.d_model, wl.d_ff)]):
+            codes = torch.empty((rows, cols * bits // 8), dtype=torch.uint8, device="cuda")
+            sc = torch.empty((rows, cols // 32), dtype=torch.float16, device="cuda")
+            L.export_packed(e, m, bits, codes, sc)
+            torch.cuda.synchronize()
+            w16 = C.expert_weight(wl, 0, e, ("w1", "w3", "w2")[m])
+            q, s = O.quantize(w16, bits)
+            assert np.array_equal(codes.cpu().numpy(), O.pack_codes(q, bits))
+            assert np.array_equal(sc.cpu().numpy().view(np.uint16), s.view(np.uint16))
+    L.destroy()
+
+
+# ------------------------------------------------------------ full layers
+def test_tiny_layer():
+    wl = C.TINY
+    _layer_case(wl, C.layer_tags(wl, 0), C.hidden_states(wl))
+
+
+def test_tiny_layer_residual():
+    wl = C.TINY
+    _layer_case(wl, C.layer_tags(wl, 0), C.hidden_states(wl), residual=True)
+
+
+def test_mixtral_t1_token_rule():
+    """Mixtral layer, one token per step; experts 4-7 miss and take int4 when
+    their gate is below 0.3.  Token streams chosen (by routing alone) so that
+    the int4 branch (streams 0, 3, 12, 17), a miss expert kept at fp16
+    (stream 1, gate 0.47) and a miss expert in slot 0 (stream 9) all occur."""
+    wl = C.MIXTRAL_T1
+    tags = C.layer_tags(wl, 0)
+    streams = [0, 1, 3, 9, 12, 17]
+    weights = S.device_layer_weights(wl, 0)
+    L = S.make_layer(wl, tags, weights, max_tokens=1)
+    experts = S.HostExperts(wl, 0, tags)
+    wg16 = C.router_weight(wl, 0)
+    outcomes = set()
+    for st in streams:
+        xt = C.hidden_states(wl, stream=st)
+        y, idx, w, prec = S.run_decode(L, torch.from_numpy(xt).cuda(), 1, wl.d_model, wl.top_k)
+        r, _ = S.check_routing(xt, wg16, tags, wl.top_k, wl.t1, wl.t2, idx, w, prec)
+        y_ref = O.layer_output(xt, experts, r)
+        err = S.normwise(y, y_ref).max()
+        print(f"stream {st}: idx {idx[0].tolist()} prec {prec[0].tolist()} err {err:.2e}")
+        assert err <= S.TOL
+        for e, p in zip(idx[0], prec[0]):
+            if tags[int(e)] == C.TAG_MISS_INT4:
+                outcomes.add(int(p))
+    L.destroy()
+    assert outcomes == {O.PREC_HIGH, O.PREC_LOW}
+
+
+def test_mixtral_t8_skewed():
+    wl = C.MIXTRAL_T8_SKEW
+    r, _ = _layer_case(wl, C.layer_tags(wl, 0), C.hidden_states(wl))
+    counts = np.bincount(r.idx.ravel(), minlength=wl.n_experts)
+    print("per-expert (token, slot) counts:", counts.tolist())
+
+
+def test_phi_layer_decode():
+    wl = C.PHI_STACK
+    _layer_case(wl, C.layer_tags(wl, 0), C.hidden_states(wl))
+
+
+# ------------------------------------------------------------ edge cases
+def test_ragged_shapes_all_tags():
+    """d and f not multiples of any lane chunk; K = E; every tag kind."""
+    wl = _edge("edge_ragged", 31, 192, 320, 5, 5, 3,
+               [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4, C.TAG_MISS_INT2],
+               t1=0.3, t2=0.8)
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((3, 192)).astype(np.float16)
+    _layer_case(wl, wl.fixed_tags, x)
+
+
+def test_skip_branch():
+    wl = _edge("edge_skip", 32, 256, 512, 4, 2, 5, [C.TAG_MISS_INT2] * 4)
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((5, 256)).astype(np.float16)
+    r, _ = _layer_case(wl, wl.fixed_tags, x, t1=0.0, t2=0.0)
+    assert np.all(r.prec[:, 0] == O.PREC_HIGH) and np.all(r.prec[:, 1] == O.PREC_SKIP)
+    r, _ = _layer_case(wl, wl.fixed_tags, x, t1=0.0, t2=1.0)
+    assert np.all(r.prec[:, 1] == O.PREC_LOW)
+
+
+def test_many_tokens_per_expert():
+    """Groups larger than the LDS token chunk; the decode maximum of 64."""
+    wl = _edge("edge_busy", 33, 256, 384, 2, 1, 20, [C.TAG_FP16, C.TAG_INT4])
+    rng = np.random.default_rng(5)
+    _layer_case(wl, wl.fixed_tags, rng.standard_normal((20, 256)).astype(np.float16))
+    wl = _edge("edge_max", 34, 128, 256, 4, 2, 64,
+               [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4])
+    _layer_case(wl, wl.fixed_tags, rng.standard_normal((64, 128)).astype(np.float16),
+                t1=0.4, t2=1.0)
+
+
+def test_top1():
+    wl = _edge("edge_top1", 35, 256, 256, 8, 1, 7, [C.TAG_INT4] * 8)
+    rng = np.random.default_rng(6)
+    r, _ = _layer_case(wl, wl.fixed_tags, rng.standard_normal((7, 256)).astype(np.float16))
+    assert np.all(r.w == 1.0)
+
+
+def test_deterministic():
+    wl = C.MIXTRAL_T8_SKEW
+    tags = C.layer_tags(wl, 0)
+    weights = S.device_layer_weights(wl, 0)
+    L = S.make_layer(wl, tags, weights)
+    xd = torch.from_numpy(C.hidden_states(wl)).cuda()
+    a = S.run_decode(L, xd, wl.n_tokens, wl.d_model, wl.top_k)
+    b = S.run_decode(L, xd, wl.n_tokens, wl.d_model, wl.top_k)
+    for u, v in zip(a, b):
+        assert np.array_equal(np.asarray(u).view(np.uint8), np.asarray(v).view(np.uint8))
+    L.destroy()
+
+
+def test_api_errors_on_device():
+    import paper_2411_01433_amd as P
+    wl = C.TINY
+    weights = S.device_layer_weights(wl, 0)
+    L = S.make_layer(wl, C.layer_tags(wl, 0), weights, max_tokens=4)
+    x = torch.zeros((5, wl.d_model), dtype=torch.float16, device="cuda")
+    y = torch.zeros((5, wl.d_model), dtype=torch.float32, device="cuda")
+    with pytest.raises(P.MoeError) as e:
+        L.decode_step(x, y)
+    assert e.value.status == P.MOE_EINVAL
+    with pytest.raises(P.MoeError) as e:
+        L.set_expert_precision(8, P.TAG_INT4)
+    assert e.value.status == P.MOE_EINVAL
+    with pytest.raises(P.MoeError) as e:
+        L.set_expert_precision(0, 9)
+    assert e.value.status == P.MOE_EINVAL
+    h = L.handle
+    L.destroy()
+    st = P.lib().moe_decode_step(h, 1, x.data_ptr(), y.data_ptr(), None, None, None, None)
+    assert st == P.MOE_ESTATE
