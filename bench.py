@@ -1,0 +1,287 @@
+#!/usr/bin/env python3
+"""Benchmark of the mixed-precision MoE layer on one MI355X.
+
+Default workload: one Mixtral-8x7B-shaped MoE layer (d_model 4096, d_ff
+14336, 8 SwiGLU experts, top-2) decoding one token per step; experts 0-3
+are cached fp16, experts 4-7 are cache misses served by their group-32 int4
+copy when their gate is below 0.3 (Eq. 2 rule with T1 = 0.7 at top-2).
+
+A step is one full pass of the layer (gate GEMV, top-k, Eq. 2 decision,
+work list, expert up/down projections, combine) over one token.  Steps
+cycle through R identical weight replicas at distinct addresses and 64
+distinct token vectors, all resident in HBM before timing starts, so that
+no step finds its expert weights in L2 or the Infinity Cache.
+
+Prints one JSON line on stdout (progress goes to stderr):
+  value          decode tokens/s (whole job, one GPU)
+  roofline       dominant kernel (expert up-projection): algorithmic bytes
+                 per launch / its mean duration from HIP events on the
+                 launch stream, against the 8 TB/s HBM peak
+  cpu_baseline   the float64 CPU oracle timed on the host cores on a
+                 bounded sample of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+METRIC = ("MoE-layer decode tokens/s + effective weight GB/s (% of HBM peak), 1 GPU")
+HBM_PEAK_GBPS = 8000.0
+N_STREAMS = 64
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def matrix_bytes(rows, cols, bits):
+    if bits == 16:
+        return rows * cols * 2
+    return rows * cols * bits // 8 + rows * (cols // 32) * 2
+
+
+def expert_bytes(d, f, bits):
+    return 2 * matrix_bytes(f, d, bits) + matrix_bytes(d, f, bits)
+
+
+def step_bytes(wl, idx, prec, tags):
+    """Algorithmic bytes of one step: every distinct (expert, precision) copy
+    the step streams, plus the gate; and the up-projection's share."""
+    d, f = wl.d_model, wl.d_ff
+    copies = set()
+    for e, p in zip(idx.ravel(), prec.ravel()):
+        if p == 2:
+            continue
+        bits = 16 if p == 0 else (4 if tags[int(e)] in (1, 3) else 2)
+        copies.add((int(e), bits))
+    T, K = idx.shape
+    n_pairs = int((prec != 2).sum())
+    total = sum(expert_bytes(d, f, b) for _, b in copies) + wl.n_experts * d * 2
+    up = (sum(2 * matrix_bytes(f, d, b) for _, b in copies)
+          + T * d * 2 + n_pairs * f * 2)
+    return total, up
+
+
+def cpu_info():
+    info = {"cpus_affinity": len(os.sched_getaffinity(0)), "nproc": os.cpu_count()}
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                info["model"] = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return info
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [p.get("num_threads", 0) for p in threadpool_info()
+             if p.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return 1
+
+
+def run_decode_layer(args):
+    import torch
+    import gpu_support as S
+    import paper_2411_01433_amd as P
+    from synth import configs as C
+
+    wl = C.BY_NAME[args.workload]
+    assert wl.n_layers == 1 and wl.mode == "decode"
+    dev = torch.device("cuda:0")
+    T, K, d = wl.n_tokens, wl.top_k, wl.d_model
+    tags = C.layer_tags(wl, 0)
+    R = args.replicas
+    log(f"workload {wl.name}: generating {R} weight replicas in HBM")
+    layers, keep = [], []
+    for r in range(R):
+        w = S.device_layer_weights(wl, 0, device=dev)
+        keep.append(w)
+        layers.append(S.make_layer(wl, tags, w, max_tokens=T))
+    xs = torch.from_numpy(np.stack([C.hidden_states(wl, stream=s) for s in range(N_STREAMS)])).to(dev)
+    n_all = args.warmup + args.steps
+    y = torch.empty((N_STREAMS, T, d), dtype=torch.float32, device=dev)
+    idx = torch.empty((n_all, T, K), dtype=torch.int32, device=dev)
+    gw = torch.empty((n_all, T, K), dtype=torch.float32, device=dev)
+    prec = torch.empty((n_all, T, K), dtype=torch.int8, device=dev)
+    torch.cuda.synchronize()
+
+    def step(i, r=None):
+        s = i % N_STREAMS
+        L = layers[(i % R) if r is None else r]
+        L.decode_step(xs[s], y[s], idx[i], gw[i], prec[i])
+
+    log("warmup", args.warmup)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log("timing", args.steps, "steps")
+    ev0.record()
+    for i in range(args.warmup, n_all):
+        step(i)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+
+    idx_h, prec_h = idx.cpu().numpy(), prec.cpu().numpy()
+    per = [step_bytes(wl, idx_h[i], prec_h[i], tags) for i in range(args.warmup, n_all)]
+    b_total = float(np.mean([p[0] for p in per]))
+    b_up = float(np.mean([p[1] for p in per]))
+
+    # hot number: one replica, same token (weights may sit in the MALL)
+    hot_steps = max(20, args.steps // 4)
+    for i in range(5):
+        layers[0].decode_step(xs[0], y[0], idx[0], gw[0], prec[0])
+    torch.cuda.synchronize()
+    ev0.record()
+    for i in range(hot_steps):
+        layers[0].decode_step(xs[0], y[0], idx[0], gw[0], prec[0])
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_hot = ev0.elapsed_time(ev1) / hot_steps
+
+    # stage-timed pass (events between kernels on the launch stream)
+    log("stage timing pass")
+    for L in layers:
+        L.enable_timing(True)
+    for i in range(args.warmup, n_all):
+        step(i)
+    torch.cuda.synchronize()
+    tot = np.zeros(4)
+    calls = 0
+    for L in layers:
+        t, n = L.stage_times()
+        tot += np.array(t)
+        calls += n
+        L.enable_timing(False)
+    stage_us = (tot / max(calls, 1) * 1e3).tolist()
+    up_us = stage_us[1]
+    achieved = b_up / (up_us * 1e-6) / 1e9
+
+    out = {
+        "metric": METRIC,
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+        "config": {"workload": wl.name, "d_model": d, "d_ff": wl.d_ff,
+                   "n_experts": wl.n_experts, "top_k": K, "tokens_per_step": T,
+                   "layers": 1, "weight_replicas": R, "token_streams": N_STREAMS,
+                   "tags": wl.note},
+        "effective_weight_GBps": b_total / (ms * 1e-3) / 1e9,
+        "pct_hbm_peak": 100.0 * b_total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "bytes_per_step": b_total,
+        "hot_tokens_per_s": T / (ms_hot * 1e-3),
+        "stage_us": dict(zip(["route", "up", "down_combine", "residual_rmsnorm"], stage_us)),
+        "roofline": {"bound": "hbm", "kernel": "decode_up_kernel",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "bytes_per_launch": b_up, "mean_launch_us": up_us},
+    }
+    return out, (wl, tags, xs, y, idx, gw, prec, layers)
+
+
+def parity_and_cpu(args, state, out):
+    """Check sampled steps against the oracle and time the oracle itself."""
+    import torch
+    import gpu_support as S
+    from oracle import moe_oracle as O
+    from synth import configs as C
+
+    wl, tags, xs, y, idx, gw, prec, layers = state
+    T, d = wl.n_tokens, wl.d_model
+    n_sample = min(args.cpu_tokens, N_STREAMS)
+    # device results for the sample, fresh, on replica 0
+    ys = []
+    for s in range(n_sample):
+        layers[0].decode_step(xs[s], y[s], idx[s], gw[s], prec[s])
+    torch.cuda.synchronize()
+    y_h, idx_h, w_h, prec_h = (y.cpu().numpy(), idx.cpu().numpy(), gw.cpu().numpy(),
+                              prec.cpu().numpy())
+    x_h = xs.cpu().numpy()
+    wg16 = C.router_weight(wl, 0)
+    experts = S.HostExperts(wl, 0, tags)
+    log(f"oracle: preparing experts for {n_sample} sample steps")
+    t0 = time.perf_counter()
+    routes = []
+    for s in range(n_sample):
+        r, _ = S.check_routing(x_h[s], wg16, tags, wl.top_k, wl.t1, wl.t2,
+                               idx_h[s], w_h[s], prec_h[s])
+        routes.append(r)
+        for t in range(T):
+            for k in range(wl.top_k):
+                if r.prec[t, k] != O.PREC_SKIP:
+                    experts[int(r.idx[t, k])].weights(int(r.prec[t, k]))
+    prep_s = time.perf_counter() - t0
+    log(f"oracle: timing (budget {args.cpu_seconds}s)")
+    errs = []
+    t0 = time.perf_counter()
+    done = 0
+    for s in range(n_sample):
+        r = O.route(x_h[s], wg16, tags, wl.top_k, wl.t1, wl.t2,
+                    forced_idx=routes[s].idx)
+        r.prec = routes[s].prec
+        y_ref = O.layer_output(x_h[s], experts, r)
+        done += 1
+        errs.append(float(S.normwise(y_h[s], y_ref).max()))
+        if time.perf_counter() - t0 > args.cpu_seconds:
+            break
+    dt = time.perf_counter() - t0
+    out["parity"] = {"steps_checked": done, "max_normwise_err": max(errs),
+                     "tol": S.TOL, "ok": max(errs) <= S.TOL}
+    out["cpu_baseline"] = {
+        "value": done * T / dt, "unit": "tokens/s", "cores": blas_threads(),
+        "kind": "oracle",
+        "sample": (f"{done} decode steps (token streams 0..{done - 1}) of the same "
+                   f"layer; float64 numpy oracle with the expert copies already "
+                   f"prepared ({prep_s:.1f}s, excluded)"),
+        "seconds": dt, "host": cpu_info()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--replicas", type=int, default=4)
+    ap.add_argument("--workload", default="mixtral_layer_decode_t1")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-tokens", type=int, default=16)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this library runs the layer on a "
+              "single MI355X (no multi-GPU path); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    import paper_2411_01433_amd as P
+    P.lib()
+    out, state = run_decode_layer(args)
+    if not args.no_cpu_baseline:
+        parity_and_cpu(args, state, out)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -77,8 +77,8 @@ typedef enum {
 enum { MOE_PREC_HIGH = 0, MOE_PREC_LOW = 1, MOE_PREC_SKIP = 2 };
 
 /* Layer shape and rule parameters.
- *  d_model, d_ff  multiples of 32 (the quantisation group), d_model <= 16384,
- *                 d_ff <= 65536
+ *  d_model, d_ff  multiples of 64 (two quantisation groups: one 16-byte int2
+ *                 load spans 64 weights), d_model <= 16384, d_ff <= 65536
  *  n_experts      1..64;  top_k 1..min(8, n_experts)
  *  group_size     must be 32
  *  max_tokens     largest n_tokens any call will pass (sizes the workspace);
@@ -168,6 +168,20 @@ moe_status moe_export_packed(moe_layer_t layer, int32_t expert, int32_t matrix,
  *  bits    4 or 2.  Needs no handle. */
 moe_status moe_quantize(const void* w, int64_t rows, int64_t cols, int32_t bits,
                         void* codes, void* scales, void* stream);
+
+/* Stage timing, for measurement.  While enabled, every decode / prefill call
+ * records HIP events on its stream between its kernels: stage 0 = routing
+ * and work list, 1 = expert up-projection with SwiGLU, 2 = expert
+ * down-projection with the weighted combine, 3 = the residual RMSNorm of
+ * the *_residual entry points (0 otherwise).  moe_layer_stage_times
+ * synchronises on the recorded events, returns in ms[0..3] the summed
+ * milliseconds per stage and in *n_calls the number of calls since timing
+ * was (re-)enabled, and restarts the sums.  Events cost a few microseconds
+ * per call: leave timing off outside measurement runs.  enable = 0 turns
+ * it off. */
+moe_status moe_layer_enable_timing(moe_layer_t layer, int32_t enable);
+moe_status moe_layer_stage_times(moe_layer_t layer, double* ms,
+                                 int32_t* n_calls);
 
 /* Free the handle, its workspace and its low-precision copies (synchronises
  * the device first).  The borrowed fp16 weights are not touched. */

@@ -20,7 +20,8 @@ PREC_HIGH, PREC_LOW, PREC_SKIP = 0, 1, 2
 EXPORTED = (
     "moe_layer_init", "moe_set_expert_precision", "moe_decode_step",
     "moe_decode_step_residual", "moe_prefill", "moe_prefill_residual",
-    "moe_export_packed", "moe_quantize", "moe_layer_destroy", "moe_last_error",
+    "moe_export_packed", "moe_quantize", "moe_layer_enable_timing",
+    "moe_layer_stage_times", "moe_layer_destroy", "moe_last_error",
 )
 
 
@@ -64,6 +65,9 @@ def lib() -> ctypes.CDLL:
     L.moe_prefill_residual.argtypes = res
     L.moe_export_packed.argtypes = [vp, i32, i32, i32, vp, vp, vp]
     L.moe_quantize.argtypes = [vp, i64, i64, i32, vp, vp, vp]
+    L.moe_layer_enable_timing.argtypes = [vp, i32]
+    L.moe_layer_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int32)]
     L.moe_layer_destroy.argtypes = [vp]
     L.moe_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
@@ -190,6 +194,16 @@ class MoeLayer:
             self._h, expert, matrix, bits,
             _ptr(codes, torch.uint8, (rows, cols * bits // 8), "codes"),
             _ptr(scales, torch.float16, (rows, cols // 32), "scales"), _stream(stream)))
+
+    def enable_timing(self, on: bool = True):
+        _check(lib().moe_layer_enable_timing(self._h, 1 if on else 0))
+
+    def stage_times(self):
+        """(summed ms per stage [route, up, down, combine], n_calls); resets."""
+        ms = (ctypes.c_double * 4)()
+        n = ctypes.c_int32()
+        _check(lib().moe_layer_stage_times(self._h, ms, ctypes.byref(n)))
+        return list(ms), n.value
 
     def destroy(self):
         if self._h is not None and self._h.value:

@@ -1,18 +1,32 @@
 // Decode-path expert kernels: fused dequantise-GEMV for the SwiGLU experts
-// of Eq. 1 at fp16, int4 or int2, and the weighted combine.
+// of Eq. 1 at fp16, int4 or int2, with the weighted combine fused into the
+// down-projection.
 //
-//   up:    h[p, r] = silu(W1[r,:] . x_t) * (W3[r,:] . x_t)   (fp16 out)
-//   down:  part[s, p, r] = W2[r, cols of split s] . h[p, cols of split s]
-//   combine: y[t] = sum_k w[t,k] * sum_s part[s, t*K+k]      (skip -> 0)
+//   up:    h[p, r] = silu(W1[r,:] . x_t) * (W3[r,:] . x_t)        (fp16 out)
+//   down:  y[t, r] = sum over the (token, slot) pairs p of token t of
+//                    w[p] * (W2[r,:] . h[p])                      (Eq. 1)
 //
-// One block handles one (expert, precision) work group and a tile of rows,
-// so the weights of every selected expert copy are streamed from HBM once
-// per step whatever the number of tokens routed to it.  Lanes of a wave
-// read consecutive 16-byte pieces of a row (1 KiB per wave-wide load); the
-// group's activations are staged in LDS in the element order the
-// dequantiser produces, and each lane accumulates with v_dot2_f32_f16
-// (fp16 x fp16 products are exact in fp32).  A low-precision group is
-// summed as q . x in fp32 and scaled once by its fp16 scale.
+// Block shape: a tile of output rows (8, or 4 when more than two tokens
+// share an expert copy) is shared by the 4 waves of a block; the waves split
+// the reduction dimension (wave w takes lane-chunks w, w+4, ...), so one
+// activation load of a lane serves every row of the tile (x2 matrices for
+// the up-projection).
+// Per lane and chunk a wave reads one piece per row:
+//   fp16  16 bytes =  8 weights   (chunk =  512 columns)
+//   int4   8 bytes = 16 weights   (chunk = 1024 columns, half a group)
+//   int2   4 bytes = 16 weights   (chunk = 1024 columns, half a group)
+// so each wave-wide load covers 1 KiB, 512 B or 256 B of one row.  Codes are
+// turned into fp16 pairs with the 0x6400|u == 1024+u trick, the matching
+// activation pairs are permuted in registers once per token, and
+// v_dot2_f32_f16 accumulates q.x in fp32 (exact products); a lane's half
+// group is then scaled once by its fp16 scale.
+//
+// Up-projection blocks each take one (expert, precision) work group and a
+// row tile, so every selected expert copy is streamed from HBM once per step
+// whatever the number of tokens routed to it.  Down-projection blocks each
+// take a row tile of d_model and loop over all work groups, accumulating
+// w[p] * e into the token's output row in LDS in work-list order, so the
+// combine needs no extra pass and the sum order is fixed (deterministic).
 #include "moe_internal.h"
 
 namespace moe {
@@ -21,11 +35,14 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kRowsPerWave = 2;
-constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
-constexpr int kLdsHalves = 32768;  // at most 64 KiB of staged activations
-constexpr int kMaxChunkTokens = 8;
+constexpr int kMaxChunkTokens = 8;  // tokens per register tile
 
+// Output rows per block for a token tile of up to NTMAX tokens: as many as
+// the register tile (rows x tokens x matrices accumulators) allows.
+template <int NTMAX> struct RowsOf { static constexpr int value = NTMAX <= 2 ? 8 : 4; };
+
+// Scalar-argument casts on purpose: clang's __builtin_bit_cast applied
+// directly to a vector component expression (v.y) reads component 0.
 __device__ inline f16x2 as_h2(uint32_t v) { return __builtin_bit_cast(f16x2, v); }
 
 __device__ inline float dot2(uint32_t a, uint32_t b, float acc) {
@@ -38,264 +55,204 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
-// int4 word holding elements e0..e7 (e_j at bits 4j) -> four fp16 pairs
-// (e_k, e_{k+4}) - 8, k = 0..3, using 0x6400|u == 1024 + u exactly.
-__device__ inline void dequant4(uint32_t w, uint32_t out[4]) {
-  const f16x2 bias = as_h2(0x64086408u);  // 1032
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    f16x2 v = as_h2(((w >> (4 * k)) & 0x000F000Fu) | 0x64006400u) - bias;
-    out[k] = __builtin_bit_cast(uint32_t, v);
-  }
+// low half of a | low half of b  /  high half of a | high half of b
+__device__ inline uint32_t lo_lo(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x05040100u);
+}
+__device__ inline uint32_t hi_hi(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x07060302u);
 }
 
-// int2 word holding e0..e15 (e_j at bits 2j) -> eight pairs (e_k, e_{k+8}) - 2.
-__device__ inline void dequant2(uint32_t w, uint32_t out[8]) {
-  const f16x2 bias = as_h2(0x64026402u);  // 1026
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    f16x2 v = as_h2(((w >> (2 * k)) & 0x00030003u) | 0x64006400u) - bias;
-    out[k] = __builtin_bit_cast(uint32_t, v);
-  }
-}
+// Elements per lane per chunk for each weight format.
+template <int BITS> struct Fmt;
+template <> struct Fmt<16> { static constexpr int kEpl = 8; };
+template <> struct Fmt<4> { static constexpr int kEpl = 16; };
+template <> struct Fmt<2> { static constexpr int kEpl = 16; };
 
-// Position of element j of a 16-element block in the staged layout.
+// Activations of one lane for one chunk, as the dword pairs the weight
+// pieces are dotted with.  fp16: natural order (4 dwords).  int4: per 8
+// elements (x0,x4)(x1,x5)(x2,x6)(x3,x7) (8 dwords).  int2: per 16 elements
+// (x0,x8)(x1,x9)...(x7,x15) (8 dwords).
 template <int BITS>
-__device__ inline int staged_pos(int j) {
-  if (BITS == 4) {  // per 8: x0 x4 x1 x5 x2 x6 x3 x7
-    const int b = j & 8, i = j & 7;
-    return b + (i < 4 ? 2 * i : 2 * (i - 4) + 1);
-  }
-  if (BITS == 2) return j < 8 ? 2 * j : 2 * (j - 8) + 1;  // x0 x8 x1 x9 ...
-  return j;
-}
-
-// Stage rows [j0, j0+n) of the group's pair list into LDS [nt][width]:
-// source row = perm[..]/K (token rows of x) or perm[..] (pair rows of h),
-// columns [c0, c0+width).  Rows n..nt-1 are zero.
-template <int BITS>
-__device__ void stage(f16* lds, const f16* src, int64_t ld, const int32_t* pairs,
-                      int n, int nt, int K, bool by_token, int c0, int width) {
-  const int bpr = width / 16;
-  for (int b = threadIdx.x; b < nt * bpr; b += kThreads) {
-    const int j = b / bpr, cb = (b - j * bpr) * 16;
-    u32x4 lo = {0, 0, 0, 0}, hi = {0, 0, 0, 0};
-    if (j < n) {
-      const int p = pairs[j];
-      const int64_t row = by_token ? p / K : p;
-      const u32x4* s = reinterpret_cast<const u32x4*>(src + row * ld + c0 + cb);
-      lo = s[0];
-      hi = s[1];
+__device__ inline void load_act(const f16* p, uint32_t (&a)[Fmt<BITS>::kEpl / 2]) {
+  if constexpr (BITS == 16) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+    a[0] = v.x; a[1] = v.y; a[2] = v.z; a[3] = v.w;
+  } else {
+    const u32x4 v0 = reinterpret_cast<const u32x4*>(p)[0];
+    const u32x4 v1 = reinterpret_cast<const u32x4*>(p)[1];
+    if constexpr (BITS == 4) {  // blocks of 8: dwords (x0x1)(x2x3)(x4x5)(x6x7)
+      a[0] = lo_lo(v0.x, v0.z); a[1] = hi_hi(v0.x, v0.z);
+      a[2] = lo_lo(v0.y, v0.w); a[3] = hi_hi(v0.y, v0.w);
+      a[4] = lo_lo(v1.x, v1.z); a[5] = hi_hi(v1.x, v1.z);
+      a[6] = lo_lo(v1.y, v1.w); a[7] = hi_hi(v1.y, v1.w);
+    } else {  // one block of 16: dwords d0..d7 = (x0x1)..(x14x15)
+      a[0] = lo_lo(v0.x, v1.x); a[1] = hi_hi(v0.x, v1.x);
+      a[2] = lo_lo(v0.y, v1.y); a[3] = hi_hi(v0.y, v1.y);
+      a[4] = lo_lo(v0.z, v1.z); a[5] = hi_hi(v0.z, v1.z);
+      a[6] = lo_lo(v0.w, v1.w); a[7] = hi_hi(v0.w, v1.w);
     }
-    f16x8 a = __builtin_bit_cast(f16x8, lo), c = __builtin_bit_cast(f16x8, hi);
-    f16 v[16], o[16];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) { v[i] = a[i]; v[8 + i] = c[i]; }
-#pragma unroll
-    for (int i = 0; i < 16; ++i) o[staged_pos<BITS>(i)] = v[i];
-    f16x8 oa, oc;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) { oa[i] = o[i]; oc[i] = o[8 + i]; }
-    u32x4* d = reinterpret_cast<u32x4*>(lds + j * width + cb);
-    d[0] = __builtin_bit_cast(u32x4, oa);
-    d[1] = __builtin_bit_cast(u32x4, oc);
   }
 }
 
-// Row dot products of NM matrices (same row index, same activations) for
-// kRowsPerWave rows starting at row0, columns [c0, c0+width) of rows of
-// length ld, against NT staged activation rows.  acc is per lane (partial).
-template <int BITS, int NT, int NM>
-struct RowDot;
+// One weight piece of one row for one chunk: loaded, then dequantised into
+// the fp16 pairs matching load_act, and its group scale.
+template <int BITS> struct Piece;
 
-template <int NT, int NM>
-struct RowDot<16, NT, NM> {
-  static __device__ void run(const ExpertEntry& ex, const int* mats, int row0,
-                             int64_t ld, int c0, int width, const f16* xs,
-                             float (&acc)[NM][kRowsPerWave][NT]) {
-    const int lane = threadIdx.x & 63;
-    for (int c = lane * 8; c < width; c += 64 * 8) {
-      u32x4 wv[NM][kRowsPerWave];
+template <> struct Piece<16> {
+  u32x4 v;
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, int64_t ld, int64_t col) {
+    v = *reinterpret_cast<const u32x4*>(ex.w[m] + row * ld + col);
+  }
+  __device__ inline float dot(const uint32_t (&a)[4], float acc) const {
+    acc = dot2(v.x, a[0], acc);
+    acc = dot2(v.y, a[1], acc);
+    acc = dot2(v.z, a[2], acc);
+    return dot2(v.w, a[3], acc);
+  }
+};
+
+template <> struct Piece<4> {
+  uint2 v;
+  f16 s;
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, int64_t ld, int64_t col) {
+    v = *reinterpret_cast<const uint2*>(ex.q[m] + row * (ld / 2) + col / 2);
+    s = ex.s[m][row * (ld / kGroup) + col / kGroup];
+  }
+  // word holding e0..e7 (e_j at bits 4j) -> pairs (e_k, e_{k+4}) - 8
+  static __device__ inline float dot_word(uint32_t w, const uint32_t* a, float g) {
+    const f16x2 bias = as_h2(0x64086408u);  // 1032 = 1024 + 8
 #pragma unroll
-      for (int m = 0; m < NM; ++m)
+    for (int k = 0; k < 4; ++k) {
+      const f16x2 q = as_h2(((w >> (4 * k)) & 0x000F000Fu) | 0x64006400u) - bias;
+      g = dot2(__builtin_bit_cast(uint32_t, q), a[k], g);
+    }
+    return g;
+  }
+  __device__ inline float dot(const uint32_t (&a)[8], float acc) const {
+    float g = dot_word(v.x, a, 0.0f);
+    g = dot_word(v.y, a + 4, g);
+    return fmaf((float)s, g, acc);
+  }
+};
+
+template <> struct Piece<2> {
+  uint32_t v;
+  f16 s;
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, int64_t ld, int64_t col) {
+    v = *reinterpret_cast<const uint32_t*>(ex.q[m] + row * (ld / 4) + col / 4);
+    s = ex.s[m][row * (ld / kGroup) + col / kGroup];
+  }
+  // word holding e0..e15 (e_j at bits 2j) -> pairs (e_k, e_{k+8}) - 2
+  __device__ inline float dot(const uint32_t (&a)[8], float acc) const {
+    const f16x2 bias = as_h2(0x64026402u);  // 1026 = 1024 + 2
+    float g = 0.0f;
 #pragma unroll
-        for (int i = 0; i < kRowsPerWave; ++i)
-          wv[m][i] = *reinterpret_cast<const u32x4*>(
-              ex.w[mats[m]] + (int64_t)(row0 + i) * ld + c0 + c);
+    for (int k = 0; k < 8; ++k) {
+      const f16x2 q = as_h2(((v >> (2 * k)) & 0x00030003u) | 0x64006400u) - bias;
+      g = dot2(__builtin_bit_cast(uint32_t, q), a[k], g);
+    }
+    return fmaf((float)s, g, acc);
+  }
+};
+
+// Partial dot products of this wave's chunks for ROWS rows of NM matrices
+// (matrix ids mats) against NT activation rows act_rows[t] (length ld).
+template <int BITS, int NT, int NM, int ROWS>
+__device__ inline void tile_dots(const ExpertEntry& ex, const int (&mats)[NM],
+                                 int64_t row0, int64_t ld,
+                                 const f16* const (&act_rows)[NT],
+                                 float (&acc)[NM][ROWS][NT]) {
+  constexpr int kEpl = Fmt<BITS>::kEpl;
+  constexpr int kChunk = 64 * kEpl;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n_chunks = (int)((ld + kChunk - 1) / kChunk);
+  for (int c = wave; c < n_chunks; c += kWaves) {
+    const int64_t col = (int64_t)c * kChunk + lane * kEpl;
+    if (col >= ld) continue;  // ragged last chunk (ld is a multiple of 64)
+    uint32_t a[NT][kEpl / 2];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) load_act<BITS>(act_rows[t] + col, a[t]);
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      Piece<BITS> pc[ROWS];
+#pragma unroll
+      for (int i = 0; i < ROWS; ++i) pc[i].load(ex, mats[m], row0 + i, ld, col);
+#pragma unroll
+      for (int i = 0; i < ROWS; ++i)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[m][i][t] = pc[i].dot(a[t], acc[m][i][t]);
+    }
+  }
+}
+
+// Sum the per-lane partials over the lanes of each wave and then over the
+// waves; afterwards red[kWaves*V + v] (v = (m*ROWS + i)*NT + t) holds the
+// full value.
+template <int NM, int NT, int ROWS>
+__device__ inline void block_reduce(float (&acc)[NM][ROWS][NT], float* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int V = NM * ROWS * NT;
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int i = 0; i < ROWS; ++i)
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const u32x4 xv = *reinterpret_cast<const u32x4*>(xs + t * width + c);
-#pragma unroll
-        for (int m = 0; m < NM; ++m)
-#pragma unroll
-          for (int i = 0; i < kRowsPerWave; ++i) {
-            float a = acc[m][i][t];
-            a = dot2(wv[m][i].x, xv.x, a);
-            a = dot2(wv[m][i].y, xv.y, a);
-            a = dot2(wv[m][i].z, xv.z, a);
-            a = dot2(wv[m][i].w, xv.w, a);
-            acc[m][i][t] = a;
-          }
+        const float s = wave_sum(acc[m][i][t]);
+        if (lane == 0) red[wave * V + (m * ROWS + i) * NT + t] = s;
       }
-    }
+  __syncthreads();
+  for (int v = threadIdx.x; v < V; v += kThreads) {
+    float s = red[v];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) s += red[w * V + v];
+    red[kWaves * V + v] = s;
   }
-};
-
-template <int NT, int NM>
-struct RowDot<4, NT, NM> {
-  static __device__ void run(const ExpertEntry& ex, const int* mats, int row0,
-                             int64_t ld, int c0, int width, const f16* xs,
-                             float (&acc)[NM][kRowsPerWave][NT]) {
-    const int lane = threadIdx.x & 63;
-    const int64_t ldq = ld / 2, lds_ = ld / kGroup;
-    for (int c = lane * 32; c < width; c += 64 * 32) {
-      const int64_t col = c0 + c;
-      u32x4 qv[NM][kRowsPerWave];
-      float sv[NM][kRowsPerWave];
-#pragma unroll
-      for (int m = 0; m < NM; ++m)
-#pragma unroll
-        for (int i = 0; i < kRowsPerWave; ++i) {
-          const int64_t r = row0 + i;
-          qv[m][i] = *reinterpret_cast<const u32x4*>(ex.q[mats[m]] + r * ldq + col / 2);
-          sv[m][i] = (float)ex.s[mats[m]][r * lds_ + col / kGroup];
-        }
-#pragma unroll
-      for (int m = 0; m < NM; ++m)
-#pragma unroll
-        for (int i = 0; i < kRowsPerWave; ++i) {
-          uint32_t dq[16];
-          dequant4(qv[m][i].x, dq + 0);
-          dequant4(qv[m][i].y, dq + 4);
-          dequant4(qv[m][i].z, dq + 8);
-          dequant4(qv[m][i].w, dq + 12);
-#pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            const u32x4* xp = reinterpret_cast<const u32x4*>(xs + t * width + c);
-            float g = 0.0f;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-              const u32x4 xv = xp[k];
-              g = dot2(dq[4 * k + 0], xv.x, g);
-              g = dot2(dq[4 * k + 1], xv.y, g);
-              g = dot2(dq[4 * k + 2], xv.z, g);
-              g = dot2(dq[4 * k + 3], xv.w, g);
-            }
-            acc[m][i][t] = fmaf(sv[m][i], g, acc[m][i][t]);
-          }
-        }
-    }
-  }
-};
-
-template <int NT, int NM>
-struct RowDot<2, NT, NM> {
-  static __device__ void run(const ExpertEntry& ex, const int* mats, int row0,
-                             int64_t ld, int c0, int width, const f16* xs,
-                             float (&acc)[NM][kRowsPerWave][NT]) {
-    const int lane = threadIdx.x & 63;
-    const int64_t ldq = ld / 4, lds_ = ld / kGroup;
-    for (int c = lane * 64; c < width; c += 64 * 64) {
-      const int64_t col = c0 + c;
-      u32x4 qv[NM][kRowsPerWave];
-      uint32_t sv[NM][kRowsPerWave];
-#pragma unroll
-      for (int m = 0; m < NM; ++m)
-#pragma unroll
-        for (int i = 0; i < kRowsPerWave; ++i) {
-          const int64_t r = row0 + i;
-          qv[m][i] = *reinterpret_cast<const u32x4*>(ex.q[mats[m]] + r * ldq + col / 4);
-          sv[m][i] = *reinterpret_cast<const uint32_t*>(ex.s[mats[m]] + r * lds_ + col / kGroup);
-        }
-#pragma unroll
-      for (int m = 0; m < NM; ++m)
-#pragma unroll
-        for (int i = 0; i < kRowsPerWave; ++i) {
-          const f16x2 s2 = as_h2(sv[m][i]);
-          uint32_t dq[32];
-          dequant2(qv[m][i].x, dq + 0);
-          dequant2(qv[m][i].y, dq + 8);
-          dequant2(qv[m][i].z, dq + 16);
-          dequant2(qv[m][i].w, dq + 24);
-#pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            const u32x4* xp = reinterpret_cast<const u32x4*>(xs + t * width + c);
-            float g0 = 0.0f, g1 = 0.0f;
-#pragma unroll
-            for (int k = 0; k < 2; ++k) {
-              const u32x4 xv = xp[k];
-              g0 = dot2(dq[4 * k + 0], xv.x, g0);
-              g0 = dot2(dq[4 * k + 1], xv.y, g0);
-              g0 = dot2(dq[4 * k + 2], xv.z, g0);
-              g0 = dot2(dq[4 * k + 3], xv.w, g0);
-            }
-#pragma unroll
-            for (int k = 2; k < 4; ++k) {
-              const u32x4 xv = xp[k];
-              g0 = dot2(dq[4 * k + 0], xv.x, g0);
-              g0 = dot2(dq[4 * k + 1], xv.y, g0);
-              g0 = dot2(dq[4 * k + 2], xv.z, g0);
-              g0 = dot2(dq[4 * k + 3], xv.w, g0);
-            }
-#pragma unroll
-            for (int k = 4; k < 8; ++k) {
-              const u32x4 xv = xp[k];
-              g1 = dot2(dq[4 * k + 0], xv.x, g1);
-              g1 = dot2(dq[4 * k + 1], xv.y, g1);
-              g1 = dot2(dq[4 * k + 2], xv.z, g1);
-              g1 = dot2(dq[4 * k + 3], xv.w, g1);
-            }
-            float a = fmaf((float)s2[0], g0, acc[m][i][t]);
-            acc[m][i][t] = fmaf((float)s2[1], g1, a);
-          }
-        }
-    }
-  }
-};
+  __syncthreads();
+}
 
 // ---------------------------------------------------------------- up-proj
-template <int BITS, int NT>
-__device__ void up_chunk(const ExpertEntry& ex, const int32_t* pairs, int n,
-                         const f16* x, f16* h, int d, int f, int K, int row0,
-                         f16* lds) {
-  stage<BITS>(lds, x, d, pairs, n, NT, K, true, 0, d);
-  __syncthreads();
-  float acc[2][kRowsPerWave][NT];
+template <int BITS, int NT, int ROWS>
+__device__ void up_tile(const ExpertEntry& ex, const int32_t* pairs, int n,
+                        const f16* x, f16* h, int d, int f, int K, int64_t row0,
+                        float* red) {
+  const f16* rows[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) rows[t] = x + (int64_t)(pairs[t < n ? t : 0] / K) * d;
+  float acc[2][ROWS][NT];
 #pragma unroll
   for (int m = 0; m < 2; ++m)
 #pragma unroll
-    for (int i = 0; i < kRowsPerWave; ++i)
+    for (int i = 0; i < ROWS; ++i)
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[m][i][t] = 0.0f;
   const int mats[2] = {0, 1};
-  RowDot<BITS, NT, 2>::run(ex, mats, row0, d, 0, d, lds, acc);
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int i = 0; i < kRowsPerWave; ++i)
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const float a = wave_sum(acc[0][i][t]);
-      const float b = wave_sum(acc[1][i][t]);
-      if (lane == i * NT + t && t < n) {
-        const float hv = a / (1.0f + expf(-a)) * b;
-        h[(int64_t)pairs[t] * f + row0 + i] = (f16)hv;
-      }
+  tile_dots<BITS, NT, 2, ROWS>(ex, mats, row0, d, rows, acc);
+  block_reduce<2, NT, ROWS>(acc, red);
+  const float* fin = red + kWaves * 2 * ROWS * NT;
+  for (int v = threadIdx.x; v < ROWS * NT; v += kThreads) {
+    const int i = v / NT, t = v - (v / NT) * NT;
+    if (t < n) {
+      const float a = fin[(0 * ROWS + i) * NT + t];
+      const float b = fin[(1 * ROWS + i) * NT + t];
+      h[(int64_t)pairs[t] * f + row0 + i] = (f16)(a / (1.0f + expf(-a)) * b);
     }
+  }
   __syncthreads();
 }
 
-// Token chunks of at most NTMAX (the host's bound: min(T, LDS capacity)),
-// each run by the smallest power-of-two instantiation that holds it.
 template <int BITS, int NTMAX>
 __device__ void up_group(const ExpertEntry& ex, const int32_t* pairs, int count,
-                         const f16* x, f16* h, int d, int f, int K, int row0,
-                         f16* lds) {
+                         const f16* x, f16* h, int d, int f, int K, int64_t row0,
+                         float* red) {
+  constexpr int R = RowsOf<NTMAX>::value;
   for (int j0 = 0; j0 < count; j0 += NTMAX) {
     const int n = min(NTMAX, count - j0);
-    if (NTMAX == 1 || n <= 1) up_chunk<BITS, 1>(ex, pairs + j0, n, x, h, d, f, K, row0, lds);
-    else if (NTMAX == 2 || n <= 2) up_chunk<BITS, (NTMAX < 2 ? NTMAX : 2)>(ex, pairs + j0, n, x, h, d, f, K, row0, lds);
-    else if (NTMAX == 4 || n <= 4) up_chunk<BITS, (NTMAX < 4 ? NTMAX : 4)>(ex, pairs + j0, n, x, h, d, f, K, row0, lds);
-    else up_chunk<BITS, NTMAX>(ex, pairs + j0, n, x, h, d, f, K, row0, lds);
+    if (NTMAX == 1 || n <= 1) up_tile<BITS, 1, R>(ex, pairs + j0, n, x, h, d, f, K, row0, red);
+    else if (NTMAX == 2 || n <= 2) up_tile<BITS, (NTMAX < 2 ? NTMAX : 2), R>(ex, pairs + j0, n, x, h, d, f, K, row0, red);
+    else if (NTMAX == 4 || n <= 4) up_tile<BITS, (NTMAX < 4 ? NTMAX : 4), R>(ex, pairs + j0, n, x, h, d, f, K, row0, red);
+    else up_tile<BITS, NTMAX, R>(ex, pairs + j0, n, x, h, d, f, K, row0, red);
   }
 }
 
@@ -304,128 +261,112 @@ __global__ __launch_bounds__(kThreads) void decode_up_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
     const int32_t* __restrict__ perm, const f16* __restrict__ x,
     f16* __restrict__ h, int d, int f, int K) {
-  extern __shared__ f16 lds[];
+  __shared__ float red[(kWaves + 1) * 2 * RowsOf<NTMAX>::value * NTMAX];
   if ((int)blockIdx.y >= wl->n_groups) return;
   const Group g = wl->groups[blockIdx.y];
   const ExpertEntry ex = table[g.expert];
-  const int row0 = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6) * kRowsPerWave;
+  const int64_t row0 = (int64_t)blockIdx.x * RowsOf<NTMAX>::value;
   const int32_t* pairs = perm + g.offset;
-  if (g.bits == 16) up_group<16, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, lds);
-  else if (g.bits == 4) up_group<4, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, lds);
-  else up_group<2, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, lds);
+  if (g.bits == 16) up_group<16, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, red);
+  else if (g.bits == 4) up_group<4, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, red);
+  else up_group<2, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, red);
 }
 
-// -------------------------------------------------------------- down-proj
-template <int BITS, int NT>
-__device__ void down_chunk(const ExpertEntry& ex, const int32_t* pairs, int n,
-                           const f16* h, float* part, int T, int d, int f,
-                           int K, int row0, int split, f16* lds) {
-  const int c0 = split * kSplitCols;
-  const int width = min(kSplitCols, f - c0);
-  stage<BITS>(lds, h, f, pairs, n, NT, K, false, c0, width);
-  __syncthreads();
-  float acc[1][kRowsPerWave][NT];
+// ------------------------------------------------- down-proj + combine
+template <int BITS, int NT, int ROWS>
+__device__ void down_tile(const ExpertEntry& ex, const int32_t* pairs, int n,
+                          const f16* h, const float* gate_w, int f, int K,
+                          int64_t row0, float* red, float* yacc) {
+  const f16* rows[NT];
 #pragma unroll
-  for (int i = 0; i < kRowsPerWave; ++i)
+  for (int t = 0; t < NT; ++t) rows[t] = h + (int64_t)pairs[t < n ? t : 0] * f;
+  float acc[1][ROWS][NT];
+#pragma unroll
+  for (int i = 0; i < ROWS; ++i)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[0][i][t] = 0.0f;
   const int mats[1] = {2};
-  RowDot<BITS, NT, 1>::run(ex, mats, row0, f, c0, width, lds, acc);
-  const int lane = threadIdx.x & 63;
-  float* out = part + (int64_t)split * T * K * d;
-#pragma unroll
-  for (int i = 0; i < kRowsPerWave; ++i)
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const float v = wave_sum(acc[0][i][t]);
-      if (lane == i * NT + t && t < n) out[(int64_t)pairs[t] * d + row0 + i] = v;
+  tile_dots<BITS, NT, 1, ROWS>(ex, mats, row0, f, rows, acc);
+  block_reduce<1, NT, ROWS>(acc, red);
+  const float* fin = red + kWaves * ROWS * NT;
+  for (int v = threadIdx.x; v < ROWS * NT; v += kThreads) {
+    const int i = v / NT, t = v - (v / NT) * NT;
+    if (t < n) {
+      const int p = pairs[t];
+      // a token occurs once per work group: no two threads share a cell
+      yacc[(p / K) * ROWS + i] += gate_w[p] * fin[i * NT + t];
     }
+  }
   __syncthreads();
 }
 
 template <int BITS, int NTMAX>
-__device__ void down_group(const ExpertEntry& ex, const int32_t* pairs,
-                           int count, const f16* h, float* part, int T, int d,
-                           int f, int K, int row0, int split, f16* lds) {
+__device__ void down_group(const ExpertEntry& ex, const int32_t* pairs, int count,
+                           const f16* h, const float* gate_w, int f, int K,
+                           int64_t row0, float* red, float* yacc) {
+  constexpr int R = RowsOf<NTMAX>::value;
   for (int j0 = 0; j0 < count; j0 += NTMAX) {
     const int n = min(NTMAX, count - j0);
-    if (NTMAX == 1 || n <= 1) down_chunk<BITS, 1>(ex, pairs + j0, n, h, part, T, d, f, K, row0, split, lds);
-    else if (NTMAX == 2 || n <= 2) down_chunk<BITS, (NTMAX < 2 ? NTMAX : 2)>(ex, pairs + j0, n, h, part, T, d, f, K, row0, split, lds);
-    else if (NTMAX == 4 || n <= 4) down_chunk<BITS, (NTMAX < 4 ? NTMAX : 4)>(ex, pairs + j0, n, h, part, T, d, f, K, row0, split, lds);
-    else down_chunk<BITS, NTMAX>(ex, pairs + j0, n, h, part, T, d, f, K, row0, split, lds);
+    if (NTMAX == 1 || n <= 1) down_tile<BITS, 1, R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
+    else if (NTMAX == 2 || n <= 2) down_tile<BITS, (NTMAX < 2 ? NTMAX : 2), R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
+    else if (NTMAX == 4 || n <= 4) down_tile<BITS, (NTMAX < 4 ? NTMAX : 4), R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
+    else down_tile<BITS, NTMAX, R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
   }
 }
 
+// y[t, rows] (or h_res[t, rows] += ...) for one row tile, all work groups.
 template <int NTMAX>
 __global__ __launch_bounds__(kThreads) void decode_down_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
-    const int32_t* __restrict__ perm, const f16* __restrict__ h,
-    float* __restrict__ part, int T, int d, int f, int K, int row_tiles) {
-  extern __shared__ f16 lds[];
-  if ((int)blockIdx.y >= wl->n_groups) return;
-  const Group g = wl->groups[blockIdx.y];
-  const ExpertEntry ex = table[g.expert];
-  const int tile = blockIdx.x % row_tiles;
-  const int split = blockIdx.x / row_tiles;
-  const int row0 = tile * kRowsPerBlock + (threadIdx.x >> 6) * kRowsPerWave;
-  const int32_t* pairs = perm + g.offset;
-  if (g.bits == 16) down_group<16, NTMAX>(ex, pairs, g.count, h, part, T, d, f, K, row0, split, lds);
-  else if (g.bits == 4) down_group<4, NTMAX>(ex, pairs, g.count, h, part, T, d, f, K, row0, split, lds);
-  else down_group<2, NTMAX>(ex, pairs, g.count, h, part, T, d, f, K, row0, split, lds);
-}
-
-// ---------------------------------------------------------------- combine
-__device__ inline float block_sum(float v, float* red) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int32_t* __restrict__ perm, const float* __restrict__ gate_w,
+    const f16* __restrict__ h, float* __restrict__ y, float* __restrict__ h_res,
+    int T, int d, int f, int K) {
+  constexpr int R = RowsOf<NTMAX>::value;
+  __shared__ float red[(kWaves + 1) * R * NTMAX];
+  __shared__ float yacc[kDecodeMaxTokens * R];
+  const int64_t row0 = (int64_t)blockIdx.x * R;
+  for (int v = threadIdx.x; v < T * R; v += kThreads) yacc[v] = 0.0f;
   __syncthreads();
-  if (lane == 0) red[wave] = v;
-  __syncthreads();
-  float s = 0.0f;
-  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) s += red[i];
-  return s;
-}
-
-__global__ __launch_bounds__(kThreads) void combine_decode_kernel(
-    const float* __restrict__ part, const float* __restrict__ w,
-    const int8_t* __restrict__ prec, int n_split, int T, int d, int K,
-    float* __restrict__ y, float* __restrict__ h_res, f16* __restrict__ x_next,
-    float eps) {
-  __shared__ float red[kThreads / 64];
-  const int t = blockIdx.x;
-  const int64_t split_stride = (int64_t)T * K * d;
-  float ss = 0.0f;
-  for (int c = threadIdx.x; c < d; c += blockDim.x) {
-    float acc = 0.0f;
-    for (int k = 0; k < K; ++k) {
-      const int p = t * K + k;
-      if (prec[p] == PREC_SKIP) continue;
-      float e = 0.0f;
-      for (int s = 0; s < n_split; ++s) e += part[s * split_stride + (int64_t)p * d + c];
-      acc = fmaf(w[p], e, acc);
-    }
-    if (h_res) {
-      const float v = h_res[(int64_t)t * d + c] + acc;
-      h_res[(int64_t)t * d + c] = v;
-      ss = fmaf(v, v, ss);
-    } else {
-      y[(int64_t)t * d + c] = acc;
-    }
+  const int n_groups = wl->n_groups;
+  for (int gi = 0; gi < n_groups; ++gi) {
+    const Group g = wl->groups[gi];
+    const ExpertEntry ex = table[g.expert];
+    const int32_t* pairs = perm + g.offset;
+    if (g.bits == 16) down_group<16, NTMAX>(ex, pairs, g.count, h, gate_w, f, K, row0, red, yacc);
+    else if (g.bits == 4) down_group<4, NTMAX>(ex, pairs, g.count, h, gate_w, f, K, row0, red, yacc);
+    else down_group<2, NTMAX>(ex, pairs, g.count, h, gate_w, f, K, row0, red, yacc);
   }
-  if (!h_res) return;
-  const float tot = block_sum(ss, red);
+  for (int v = threadIdx.x; v < T * R; v += kThreads) {
+    const int t = v / R, i = v - t * R;
+    const int64_t o = (int64_t)t * d + row0 + i;
+    if (h_res) h_res[o] += yacc[v];
+    else y[o] = yacc[v];
+  }
+}
+
+// ------------------------------------------------------ residual RMSNorm
+__global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
+    const float* __restrict__ h_res, f16* __restrict__ x_next, int d, float eps) {
+  __shared__ float red[kWaves];
+  const int64_t base = (int64_t)blockIdx.x * d;
+  float ss = 0.0f;
+  for (int c = threadIdx.x; c < d; c += kThreads) {
+    const float v = h_res[base + c];
+    ss = fmaf(v, v, ss);
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) tot += red[w];
   const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += blockDim.x)
-    x_next[(int64_t)t * d + c] = (f16)(h_res[(int64_t)t * d + c] * r);
+  for (int c = threadIdx.x; c < d; c += kThreads)
+    x_next[base + c] = (f16)(h_res[base + c] * r);
 }
 
-int chunk_tokens(int width) {
-  int c = kLdsHalves / width;
-  return c >= kMaxChunkTokens ? kMaxChunkTokens : (c >= 4 ? 4 : (c >= 2 ? 2 : 1));
-}
-
-int lds_tokens(int chunk, int T) {
-  const int n = T < chunk ? T : chunk;
+int nt_max(int T) {
+  const int n = T < kMaxChunkTokens ? T : kMaxChunkTokens;
   return n <= 1 ? 1 : (n <= 2 ? 2 : (n <= 4 ? 4 : 8));
 }
 
@@ -434,43 +375,35 @@ int lds_tokens(int chunk, int T) {
 hipError_t launch_decode_up(const ExpertEntry* table, const WorkList* wl,
                             const int32_t* perm, const f16* x, f16* h, int T,
                             int d, int f, int K, int max_groups, hipStream_t s) {
-  const int nt = lds_tokens(chunk_tokens(d), T);
-  const size_t lds = (size_t)nt * d * sizeof(f16);
-  dim3 grid(f / kRowsPerBlock, max_groups);
+  const int nt = nt_max(T);
+  dim3 grid(f / (nt <= 2 ? RowsOf<1>::value : RowsOf<8>::value), max_groups);
   switch (nt) {
-    case 1: decode_up_kernel<1><<<grid, kThreads, lds, s>>>(table, wl, perm, x, h, d, f, K); break;
-    case 2: decode_up_kernel<2><<<grid, kThreads, lds, s>>>(table, wl, perm, x, h, d, f, K); break;
-    case 4: decode_up_kernel<4><<<grid, kThreads, lds, s>>>(table, wl, perm, x, h, d, f, K); break;
-    default: decode_up_kernel<8><<<grid, kThreads, lds, s>>>(table, wl, perm, x, h, d, f, K); break;
+    case 1: decode_up_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
+    case 2: decode_up_kernel<2><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
+    case 4: decode_up_kernel<4><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
+    default: decode_up_kernel<8><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
-                              const int32_t* perm, const f16* h, float* part,
-                              int T, int d, int f, int K, int max_groups,
-                              hipStream_t s) {
-  const int nt = lds_tokens(chunk_tokens(kSplitCols), T);
-  const int width = f < kSplitCols ? f : kSplitCols;
-  const size_t lds = (size_t)nt * width * sizeof(f16);
-  const int row_tiles = d / kRowsPerBlock;
-  const int n_split = (f + kSplitCols - 1) / kSplitCols;
-  dim3 grid(row_tiles * n_split, max_groups);
+                              const int32_t* perm, const float* gate_w,
+                              const f16* h, float* y, float* h_res, int T, int d,
+                              int f, int K, hipStream_t s) {
+  const int nt = nt_max(T);
+  dim3 grid(d / (nt <= 2 ? RowsOf<1>::value : RowsOf<8>::value));
   switch (nt) {
-    case 1: decode_down_kernel<1><<<grid, kThreads, lds, s>>>(table, wl, perm, h, part, T, d, f, K, row_tiles); break;
-    case 2: decode_down_kernel<2><<<grid, kThreads, lds, s>>>(table, wl, perm, h, part, T, d, f, K, row_tiles); break;
-    case 4: decode_down_kernel<4><<<grid, kThreads, lds, s>>>(table, wl, perm, h, part, T, d, f, K, row_tiles); break;
-    default: decode_down_kernel<8><<<grid, kThreads, lds, s>>>(table, wl, perm, h, part, T, d, f, K, row_tiles); break;
+    case 1: decode_down_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
+    case 2: decode_down_kernel<2><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
+    case 4: decode_down_kernel<4><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
+    default: decode_down_kernel<8><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_combine_decode(const float* part, const float* w,
-                                 const int8_t* prec, int n_split, int T, int d,
-                                 int K, float* y, float* h_res, f16* x_next,
-                                 float eps, hipStream_t s) {
-  combine_decode_kernel<<<T, kThreads, 0, s>>>(part, w, prec, n_split, T, d, K,
-                                               y, h_res, x_next, eps);
+hipError_t launch_rmsnorm(const float* h_res, f16* x_next, int T, int d,
+                          float eps, hipStream_t s) {
+  rmsnorm_kernel<<<T, kThreads, 0, s>>>(h_res, x_next, d, eps);
   return hipGetLastError();
 }
 

@@ -64,10 +64,13 @@ struct moe_layer {
   float* d_w = nullptr;
   int8_t* d_prec = nullptr;
   f16* d_h = nullptr;       // [max_tokens*K, f]
-  float* d_part = nullptr;  // decode: [n_split, min(max_tokens,64)*K, d]
   f16* d_xperm = nullptr;   // prefill: [max_tokens*K, d]
   float* d_eperm = nullptr; // prefill: [max_tokens*K, d]
   void* arena = nullptr;
+  // stage timing (measurement only): 5 events per recorded call
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
 };
 
 namespace {
@@ -98,8 +101,6 @@ moe_status check_desc(const moe_layer_desc* d) {
   if (d->flags != 0) return fail(MOE_EINVAL, "flags must be 0");
   return MOE_OK;
 }
-
-int n_split_of(int f) { return (f + kSplitCols - 1) / kSplitCols; }
 
 moe_status check_call(moe_layer* l, int32_t n_tokens, int32_t limit,
                       const void* x, const void* out0, const void* out1) {
@@ -147,6 +148,22 @@ int max_groups_of(moe_layer* l, int T) {
   return a < b ? a : b;
 }
 
+// Record event number `slot` (0..4) of the current call when timing is on.
+hipError_t mark(moe_layer* l, int slot, hipStream_t s) {
+  if (!l->timing) return hipSuccess;
+  if (slot == 0 && l->ev_used + 5 > l->ev_pool.size()) {
+    for (int i = 0; i < 5; ++i) {
+      hipEvent_t e;
+      hipError_t he = hipEventCreate(&e);
+      if (he != hipSuccess) return he;
+      l->ev_pool.push_back(e);
+    }
+  }
+  const size_t at = l->ev_used + slot;
+  if (slot == 4) l->ev_used += 5;
+  return hipEventRecord(l->ev_pool[at], s);
+}
+
 moe_status decode_impl(moe_layer* l, int32_t T, const void* x, float* y,
                        float* h_res, void* x_next, int32_t* idx, float* w,
                        int8_t* prec, void* stream) {
@@ -159,15 +176,20 @@ moe_status decode_impl(moe_layer* l, int32_t T, const void* x, float* y,
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
   const int mg = max_groups_of(l, T);
+  HIP_TRY(mark(l, 0, s), "timing event");
   HIP_TRY(launch_route_decode(route_params(l, T, x), route_out(l, idx, w, prec),
                               l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
+  HIP_TRY(mark(l, 1, s), "timing event");
   HIP_TRY(launch_decode_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
                            l->d_h, T, d, f, K, mg, s), "up kernel launch");
-  HIP_TRY(launch_decode_down(l->d_table, l->d_wl, l->d_perm, l->d_h, l->d_part, T,
-                             d, f, K, mg, s), "down kernel launch");
-  HIP_TRY(launch_combine_decode(l->d_part, l->d_w, l->d_prec, n_split_of(f), T, d, K,
-                                y, h_res, static_cast<f16*>(x_next),
-                                l->desc.rms_eps, s), "combine kernel launch");
+  HIP_TRY(mark(l, 2, s), "timing event");
+  HIP_TRY(launch_decode_down(l->d_table, l->d_wl, l->d_perm, l->d_w, l->d_h, y, h_res,
+                             T, d, f, K, s), "down kernel launch");
+  HIP_TRY(mark(l, 3, s), "timing event");
+  if (h_res)
+    HIP_TRY(launch_rmsnorm(h_res, static_cast<f16*>(x_next), T, d, l->desc.rms_eps, s),
+            "rmsnorm kernel launch");
+  HIP_TRY(mark(l, 4, s), "timing event");
   return MOE_OK;
 }
 
@@ -183,18 +205,25 @@ moe_status prefill_impl(moe_layer* l, int32_t T, const void* x, float* y,
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
   const int mg = max_groups_of(l, T);
+  HIP_TRY(mark(l, 0, s), "timing event");
   HIP_TRY(launch_route_prefill(route_params(l, T, x), route_out(l, idx, w, prec),
                                l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
-  HIP_TRY(launch_prefill_experts(l->d_table, l->d_wl, l->d_perm,
-                                 static_cast<const f16*>(x), l->d_xperm, l->d_h,
-                                 l->d_eperm, T, d, f, K, mg, s), "prefill expert launch");
+  HIP_TRY(mark(l, 1, s), "timing event");
+  HIP_TRY(launch_prefill_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
+                            l->d_xperm, l->d_h, T, d, f, K, mg, s), "prefill up launch");
+  HIP_TRY(mark(l, 2, s), "timing event");
+  HIP_TRY(launch_prefill_down(l->d_table, l->d_wl, l->d_h, l->d_eperm, T, d, f, K, mg, s),
+          "prefill down launch");
+  HIP_TRY(mark(l, 3, s), "timing event");
   HIP_TRY(launch_combine_prefill(l->d_eperm, l->d_pos, l->d_w, l->d_prec, T, d, K, y,
                                  h_res, static_cast<f16*>(x_next), l->desc.rms_eps, s),
           "combine kernel launch");
+  HIP_TRY(mark(l, 4, s), "timing event");
   return MOE_OK;
 }
 
 void free_layer(moe_layer* l) {
+  for (hipEvent_t e : l->ev_pool) (void)hipEventDestroy(e);
   for (void* p : l->owned) (void)hipFree(p);
   if (l->arena) (void)hipFree(l->arena);
   delete l;
@@ -229,7 +258,6 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   l->w_router = static_cast<const f16*>(w_router);
   const int E = desc->n_experts, K = desc->top_k, d = desc->d_model, f = desc->d_ff;
   const int64_t M = desc->max_tokens;
-  const int64_t Md = M < kDecodeMaxTokens ? M : kDecodeMaxTokens;
   l->host_table.resize(E);
   l->low_q.resize(E);
   l->low_s.resize(E);
@@ -254,7 +282,6 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   const size_t o_w = off;     off += al(sizeof(float) * M * K);
   const size_t o_prec = off;  off += al(sizeof(int8_t) * M * K);
   const size_t o_h = off;     off += al(sizeof(f16) * M * K * f);
-  const size_t o_part = off;  off += al(sizeof(float) * n_split_of(f) * Md * K * d);
   const size_t o_xp = off;    off += al(sizeof(f16) * M * K * d);
   const size_t o_ep = off;    off += al(sizeof(float) * M * K * d);
   he = hipMalloc(&l->arena, off);
@@ -271,7 +298,6 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   l->d_w = reinterpret_cast<float*>(base + o_w);
   l->d_prec = reinterpret_cast<int8_t*>(base + o_prec);
   l->d_h = reinterpret_cast<f16*>(base + o_h);
-  l->d_part = reinterpret_cast<float*>(base + o_part);
   l->d_xperm = reinterpret_cast<f16*>(base + o_xp);
   l->d_eperm = reinterpret_cast<float*>(base + o_ep);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -402,6 +428,37 @@ moe_status moe_quantize(const void* w, int64_t rows, int64_t cols, int32_t bits,
   HIP_TRY(launch_quantize(static_cast<const f16*>(w), rows, cols, bits,
                           static_cast<uint8_t*>(codes), static_cast<f16*>(scales),
                           static_cast<hipStream_t>(stream)), "quantize kernel launch");
+  return MOE_OK;
+}
+
+moe_status moe_layer_enable_timing(moe_layer_t l, int32_t enable) {
+  g_err.clear();
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  l->timing = enable != 0;
+  l->ev_used = 0;
+  return MOE_OK;
+}
+
+moe_status moe_layer_stage_times(moe_layer_t l, double* ms, int32_t* n_calls) {
+  g_err.clear();
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  if (!ms || !n_calls) return fail(MOE_EINVAL, "ms and n_calls must not be NULL");
+  for (int i = 0; i < 4; ++i) ms[i] = 0.0;
+  const size_t calls = l->ev_used / 5;
+  if (calls) {
+    moe_status st = set_device(l);
+    if (st != MOE_OK) return st;
+    HIP_TRY(hipEventSynchronize(l->ev_pool[l->ev_used - 1]), "timing synchronize");
+  }
+  for (size_t c = 0; c < calls; ++c)
+    for (int i = 0; i < 4; ++i) {
+      float t = 0.0f;
+      HIP_TRY(hipEventElapsedTime(&t, l->ev_pool[5 * c + i], l->ev_pool[5 * c + i + 1]),
+              "timing elapsed");
+      ms[i] += t;
+    }
+  *n_calls = (int32_t)calls;
+  l->ev_used = 0;
   return MOE_OK;
 }
 

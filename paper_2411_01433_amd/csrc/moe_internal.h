@@ -20,7 +20,6 @@ constexpr int kMaxExperts = 64;
 constexpr int kMaxTopK = 8;
 constexpr int kMaxKeys = 2 * kMaxExperts;  // (expert, high|low) work groups
 constexpr int kDecodeMaxTokens = 64;
-constexpr int kSplitCols = 4096;    // K-split width of the decode down-proj
 
 enum { PREC_HIGH = 0, PREC_LOW = 1, PREC_SKIP = 2 };
 enum { TAG_FP16 = 0, TAG_INT4 = 1, TAG_INT2 = 2, TAG_MISS_INT4 = 3,
@@ -85,18 +84,18 @@ hipError_t launch_decode_up(const ExpertEntry* table, const WorkList* wl,
                             int T, int d, int f, int K, int max_groups,
                             hipStream_t s);
 hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
-                              const int32_t* perm, const f16* h, float* part,
-                              int T, int d, int f, int K, int max_groups,
-                              hipStream_t s);
-hipError_t launch_combine_decode(const float* part, const float* w,
-                                 const int8_t* prec, int n_split, int T, int d,
-                                 int K, float* y, float* h_res, f16* x_next,
-                                 float eps, hipStream_t s);
-hipError_t launch_prefill_experts(const ExpertEntry* table, const WorkList* wl,
-                                  const int32_t* perm, const f16* x,
-                                  f16* x_perm, f16* h_perm, float* e_perm,
-                                  int T, int d, int f, int K, int max_groups,
-                                  hipStream_t s);
+                              const int32_t* perm, const float* gate_w,
+                              const f16* h, float* y, float* h_res, int T, int d,
+                              int f, int K, hipStream_t s);
+hipError_t launch_rmsnorm(const float* h_res, f16* x_next, int T, int d,
+                          float eps, hipStream_t s);
+hipError_t launch_prefill_up(const ExpertEntry* table, const WorkList* wl,
+                             const int32_t* perm, const f16* x, f16* x_perm,
+                             f16* h_perm, int T, int d, int f, int K,
+                             int max_groups, hipStream_t s);
+hipError_t launch_prefill_down(const ExpertEntry* table, const WorkList* wl,
+                               const f16* h_perm, float* e_perm, int T, int d,
+                               int f, int K, int max_groups, hipStream_t s);
 hipError_t launch_combine_prefill(const float* e_perm, const int32_t* pos,
                                   const float* w, const int8_t* prec, int T,
                                   int d, int K, float* y, float* h_res,

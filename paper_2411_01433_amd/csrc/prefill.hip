@@ -3,9 +3,13 @@
 
 namespace moe {
 
-hipError_t launch_prefill_experts(const ExpertEntry*, const WorkList*, const int32_t*,
-                                  const f16*, f16*, f16*, float*, int, int, int, int,
-                                  int, hipStream_t) {
+hipError_t launch_prefill_up(const ExpertEntry*, const WorkList*, const int32_t*,
+                             const f16*, f16*, f16*, int, int, int, int, int, hipStream_t) {
+  return hipErrorNotSupported;
+}
+
+hipError_t launch_prefill_down(const ExpertEntry*, const WorkList*, const f16*, float*,
+                               int, int, int, int, int, hipStream_t) {
   return hipErrorNotSupported;
 }
 

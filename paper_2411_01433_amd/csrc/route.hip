@@ -20,6 +20,14 @@ constexpr int kRouteThreads = 1024;
 constexpr int kPrefillTokPerBlock = 8;
 constexpr int kPrefillThreads = 256;
 
+// fp16-pair dot product with fp32 accumulation.  The operands are taken
+// as scalars on purpose: clang's __builtin_bit_cast applied directly to a
+// vector component expression (v.y) reads component 0.
+__device__ inline float dot2(uint32_t a, uint32_t b, float acc) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, a),
+                                __builtin_bit_cast(f16x2, b), acc, false);
+}
+
 __device__ inline float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -27,8 +35,11 @@ __device__ inline float wave_sum(float v) {
 }
 
 // Dot products of tokens [t0, t1) against all E gate rows; one wave per
-// (token, expert) pair, 8 fp16 per lane per step.  Results go to lg[t-t0][e].
+// (token, expert) pair, 8 fp16 per lane per 512-column chunk.  A batch of 8
+// chunks is loaded before any arithmetic so the loads overlap.  Results go
+// to lg[t-t0][e].
 __device__ void gate_logits(const RouteParams& p, int t0, int t1, float* lg) {
+  constexpr int kBatch = 8;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int n_waves = blockDim.x >> 6;
@@ -39,13 +50,21 @@ __device__ void gate_logits(const RouteParams& p, int t0, int t1, float* lg) {
     const f16* xr = p.x + (int64_t)(t0 + tl) * p.d;
     const f16* gr = p.wg + (int64_t)e * p.d;
     float acc = 0.0f;
-    for (int c = lane * 8; c < p.d; c += 64 * 8) {
-      f16x8 a = __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(xr + c));
-      f16x8 b = __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(gr + c));
+    for (int c0 = 0; c0 < p.d; c0 += kBatch * 512) {
+      u32x4 a[kBatch], b[kBatch];
 #pragma unroll
-      for (int j = 0; j < 8; j += 2)
-        acc = __builtin_amdgcn_fdot2(f16x2{a[j], a[j + 1]},
-                                     f16x2{b[j], b[j + 1]}, acc, false);
+      for (int j = 0; j < kBatch; ++j) {
+        const int c = c0 + j * 512 + lane * 8;
+        a[j] = c < p.d ? *reinterpret_cast<const u32x4*>(xr + c) : u32x4{0, 0, 0, 0};
+        b[j] = c < p.d ? *reinterpret_cast<const u32x4*>(gr + c) : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        acc = dot2(a[j].x, b[j].x, acc);
+        acc = dot2(a[j].y, b[j].y, acc);
+        acc = dot2(a[j].z, b[j].z, acc);
+        acc = dot2(a[j].w, b[j].w, acc);
+      }
     }
     acc = wave_sum(acc);
     if (lane == 0) lg[tl * p.E + e] = acc;
