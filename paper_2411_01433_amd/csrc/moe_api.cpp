@@ -1,6 +1,6 @@
 // Host runtime behind include/moe.h: argument validation, handle registry,
 // workspace, expert table and the launch sequence of one layer call.
-#include "../../include/moe.h"
+#include "moe.h"
 
 #include <hip/hip_runtime.h>
 

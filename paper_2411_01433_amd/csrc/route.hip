@@ -71,9 +71,10 @@ __device__ void gate_logits(const RouteParams& p, int t0, int t1, float* lg) {
   }
 }
 
-// top-k, softmax over the selected logits and the Eq. 2 rule for one token.
+// top-k, softmax over the selected logits and the Eq. 2 rule for one token;
+// tags[e] is the expert table's tag column staged in LDS.
 __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
-                             RouteOut o) {
+                             const int* tags, RouteOut o) {
   int sel[kMaxTopK];
   float ls[kMaxTopK];
   uint64_t taken = 0;  // E <= 64
@@ -102,7 +103,7 @@ __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
   for (int k = 0; k < p.K; ++k) {
     const float w = ex[k] / z;
     const int e = sel[k];
-    const int tag = p.table[e].tag;
+    const int tag = tags[e];
     int prec;
     if (tag == TAG_FP16) {
       prec = PREC_HIGH;
@@ -127,8 +128,8 @@ __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
 // Stable counting sort of all T*K pairs by key = expert*2 + (low ? 1 : 0)
 // (skipped pairs get no key).  Run by one whole block.
 __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
-                               const int8_t* prec, WorkList* wl,
-                               int32_t* perm, int32_t* pos) {
+                               const int8_t* prec, const int* low_bits,
+                               WorkList* wl, int32_t* perm, int32_t* pos) {
   __shared__ int cnt[kMaxKeys];
   __shared__ int base[kMaxKeys];
   __shared__ int chunk_keys[kRouteThreads];
@@ -152,7 +153,7 @@ __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
         const int e = k >> 1;
         Group g;
         g.expert = e;
-        g.bits = (k & 1) ? p.table[e].low_bits : 16;
+        g.bits = (k & 1) ? low_bits[e] : 16;
         g.offset = off;
         g.count = c;
         wl->groups[ng++] = g;
@@ -190,33 +191,49 @@ __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
   }
 }
 
+// Expert tags and low-copy widths into LDS (issued before the gate loads so
+// the two memory round trips overlap).
+__device__ inline void stage_table(const RouteParams& p, int* tags, int* low_bits) {
+  for (int e = threadIdx.x; e < p.E; e += blockDim.x) {
+    tags[e] = p.table[e].tag;
+    low_bits[e] = p.table[e].low_bits;
+  }
+}
+
 // Decode: one block routes every token and builds the work list.
 __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
     RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
   __shared__ float lg[kDecodeMaxTokens * kMaxExperts];
+  __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
+  stage_table(p, tags, low_bits);
   gate_logits(p, 0, p.T, lg);
   __syncthreads();
   for (int t = threadIdx.x; t < p.T; t += blockDim.x)
-    decide_token(p, t, lg + t * p.E, o);
+    decide_token(p, t, lg + t * p.E, tags, o);
   __syncthreads();
-  build_worklist(p, o.idx, o.prec, wl, perm, pos);
+  build_worklist(p, o.idx, o.prec, low_bits, wl, perm, pos);
 }
 
 // Prefill: many blocks route their tokens; a second kernel builds the list.
 __global__ __launch_bounds__(kPrefillThreads) void route_tokens_kernel(
     RouteParams p, RouteOut o) {
   __shared__ float lg[kPrefillTokPerBlock * kMaxExperts];
+  __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
   const int t0 = blockIdx.x * kPrefillTokPerBlock;
   const int t1 = min(t0 + kPrefillTokPerBlock, p.T);
+  stage_table(p, tags, low_bits);
   gate_logits(p, t0, t1, lg);
   __syncthreads();
   for (int t = t0 + (int)threadIdx.x; t < t1; t += blockDim.x)
-    decide_token(p, t, lg + (t - t0) * p.E, o);
+    decide_token(p, t, lg + (t - t0) * p.E, tags, o);
 }
 
 __global__ __launch_bounds__(kRouteThreads) void worklist_kernel(
     RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
-  build_worklist(p, o.idx, o.prec, wl, perm, pos);
+  __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
+  stage_table(p, tags, low_bits);
+  __syncthreads();
+  build_worklist(p, o.idx, o.prec, low_bits, wl, perm, pos);
 }
 
 }  // namespace
