@@ -64,8 +64,7 @@ struct moe_layer {
   float* d_w = nullptr;
   int8_t* d_prec = nullptr;
   f16* d_h = nullptr;       // [max_tokens*K, f]
-  f16* d_xperm = nullptr;   // prefill: [max_tokens*K, d]
-  float* d_eperm = nullptr; // prefill: [max_tokens*K, d]
+  float* d_eperm = nullptr; // prefill expert outputs in group order: [max_tokens*K, d]
   void* arena = nullptr;
   // stage timing (measurement only): 5 events per recorded call
   bool timing = false;
@@ -210,7 +209,7 @@ moe_status prefill_impl(moe_layer* l, int32_t T, const void* x, float* y,
                                l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
   HIP_TRY(mark(l, 1, s), "timing event");
   HIP_TRY(launch_prefill_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
-                            l->d_xperm, l->d_h, T, d, f, K, mg, s), "prefill up launch");
+                            l->d_h, T, d, f, K, mg, s), "prefill up launch");
   HIP_TRY(mark(l, 2, s), "timing event");
   HIP_TRY(launch_prefill_down(l->d_table, l->d_wl, l->d_h, l->d_eperm, T, d, f, K, mg, s),
           "prefill down launch");
@@ -282,7 +281,6 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   const size_t o_w = off;     off += al(sizeof(float) * M * K);
   const size_t o_prec = off;  off += al(sizeof(int8_t) * M * K);
   const size_t o_h = off;     off += al(sizeof(f16) * M * K * f);
-  const size_t o_xp = off;    off += al(sizeof(f16) * M * K * d);
   const size_t o_ep = off;    off += al(sizeof(float) * M * K * d);
   he = hipMalloc(&l->arena, off);
   if (he != hipSuccess) {
@@ -298,7 +296,6 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   l->d_w = reinterpret_cast<float*>(base + o_w);
   l->d_prec = reinterpret_cast<int8_t*>(base + o_prec);
   l->d_h = reinterpret_cast<f16*>(base + o_h);
-  l->d_xperm = reinterpret_cast<f16*>(base + o_xp);
   l->d_eperm = reinterpret_cast<float*>(base + o_ep);
   hipStream_t s = static_cast<hipStream_t>(stream);
   he = hipMemcpyAsync(l->d_table, l->host_table.data(), sizeof(ExpertEntry) * E,

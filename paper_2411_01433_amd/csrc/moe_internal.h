@@ -91,9 +91,9 @@ hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
 hipError_t launch_rmsnorm(const float* h_res, f16* x_next, int T, int d,
                           float eps, hipStream_t s);
 hipError_t launch_prefill_up(const ExpertEntry* table, const WorkList* wl,
-                             const int32_t* perm, const f16* x, f16* x_perm,
-                             f16* h_perm, int T, int d, int f, int K,
-                             int max_groups, hipStream_t s);
+                             const int32_t* perm, const f16* x, f16* h_perm,
+                             int T, int d, int f, int K, int max_groups,
+                             hipStream_t s);
 hipError_t launch_prefill_down(const ExpertEntry* table, const WorkList* wl,
                                const f16* h_perm, float* e_perm, int T, int d,
                                int f, int K, int max_groups, hipStream_t s);

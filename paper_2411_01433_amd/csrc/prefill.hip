@@ -1,22 +1,380 @@
-// Prefill path (MFMA grouped GEMM): placeholder until the kernels land.
+// Prefill path: the experts of Eq. 1 as an MFMA grouped GEMM with the
+// low-precision copies dequantised in registers, then the weighted combine.
+//
+//   up:    H[j, r] = silu(X_g W1^T)[j, r] * (X_g W3^T)[j, r]     (fp16 out)
+//   down:  E[j, r] = (H_g W2^T)[j, r]                             (fp32 out)
+//   combine: y[t] = sum_k w[t,k] * E[pos(t,k)]                    (Eq. 1)
+//
+// X_g is the group's tokens: the router's stable counting sort lists every
+// (token, slot) pair of a work group contiguously (perm[]); the up kernel
+// gathers those token rows while staging them in LDS (the permute step),
+// and H / E are kept in that group order (row j of the group at position
+// offset + j), so the down kernel reads contiguous rows and the combine
+// finds each pair through pos[].
+//
+// Tiling (v_mfma_f32_16x16x32_f16: lane l holds A[l%16][8(l/16)+i],
+// B[8(l/16)+i][l%16] and C[4(l/16)+i][l%16]): M = tokens (A = activations
+// from LDS, up to 128 per pass = 8 tiles), N = weight rows (B = weight
+// rows, each lane's 8 k-values contiguous in memory), K = reduction dim in
+// stages of 128.  A block of 4 waves owns 4 x ROWS_W weight rows; each wave
+// owns ROWS_W rows for all the pass's tokens, so every weight element is
+// fetched from HBM once per pass and used 128 times.  Weight fragments are
+// loaded straight into registers with nontemporal loads:
+//   fp16: lane group g (= l/16) reads 16 B at k = 32s + 8g for step s;
+//   int4: lane group g reads the whole 16 B group g of the stage (32 codes)
+//         and step s uses its word s;
+//   int2: lane group g reads the 8 B group g and step s uses half-word s;
+// low codes are turned into fp16 with the 0x6400|u == 1024+u trick and
+// scaled by the group's fp16 scale (w = fp16(q*s)); the pair order this
+// produces, (e0,e4)(e1,e5)(e2,e6)(e3,e7), is matched by staging the
+// activations in LDS with the same permutation inside every 8 elements.
 #include "moe_internal.h"
 
 namespace moe {
 
-hipError_t launch_prefill_up(const ExpertEntry*, const WorkList*, const int32_t*,
-                             const f16*, f16*, f16*, int, int, int, int, int, hipStream_t) {
-  return hipErrorNotSupported;
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
+constexpr int kStageK = 128;              // reduction columns per stage
+constexpr int kPassTok = 128;             // tokens per pass (8 MFMA tiles)
+constexpr int kTokTiles = kPassTok / 16;
+constexpr int kLdsRow = kStageK + 8;      // halves per staged row (16 B pad)
+constexpr int kUpRowsW = 32;              // weight rows per wave, up-projection
+constexpr int kDownRowsW = 16;            // weight rows per wave, down-projection
+
+typedef __attribute__((address_space(1))) const u32x4* gvec4;
+
+template <class T>
+__device__ inline const __attribute__((address_space(1))) T* gmem(const T* p) {
+  return (const __attribute__((address_space(1))) T*)p;
 }
 
-hipError_t launch_prefill_down(const ExpertEntry*, const WorkList*, const f16*, float*,
-                               int, int, int, int, int, hipStream_t) {
-  return hipErrorNotSupported;
+__device__ inline f16x2 as_h2(uint32_t v) { return __builtin_bit_cast(f16x2, v); }
+__device__ inline uint32_t as_u32(f16x2 v) { return __builtin_bit_cast(uint32_t, v); }
+
+__device__ inline f16x8 pack8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  return __builtin_bit_cast(f16x8, u32x4{a, b, c, d});
 }
 
-hipError_t launch_combine_prefill(const float*, const int32_t*, const float*,
-                                  const int8_t*, int, int, int, float*, float*, f16*,
-                                  float, hipStream_t) {
-  return hipErrorNotSupported;
+// Position of element i of an 8-block in the staged activation layout for
+// low-precision groups: x0 x4 x1 x5 x2 x6 x3 x7.
+__device__ inline int perm8(int i) { return i < 4 ? 2 * i : 2 * (i - 4) + 1; }
+
+// Stage rows [j0, j0 + n) of the group's activation matrix, columns
+// [k0, k0 + 128), into LDS [128][kLdsRow]; rows beyond n and columns beyond
+// ld are zero.  Source row of group row j: perm[off + j] / K (token rows of
+// x) or off + j (rows of H, already in group order).
+template <bool PERMUTE>
+__device__ void stage_act(f16* lds, const f16* src, int64_t ld, const int32_t* perm,
+                          int off, int j0, int n, int K, bool gather, int64_t k0) {
+  for (int e = threadIdx.x; e < kPassTok * (kStageK / 8); e += kThreads) {
+    const int r = e >> 4, piece = e & 15;
+    const int64_t col = k0 + piece * 8;
+    u32x4 v = {0, 0, 0, 0};
+    if (r < n && col < ld) {
+      const int64_t row = gather ? perm[off + j0 + r] / K : (int64_t)(off + j0 + r);
+      v = *reinterpret_cast<const u32x4*>(src + row * ld + col);
+    }
+    if (PERMUTE) {
+      const f16x8 a = __builtin_bit_cast(f16x8, v);
+      f16x8 b;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) b[perm8(i)] = a[i];
+      v = __builtin_bit_cast(u32x4, b);
+    }
+    *reinterpret_cast<u32x4*>(lds + r * kLdsRow + piece * 8) = v;
+  }
+}
+
+// A fragment (activations) of token tile tt for step s of the stage.
+template <int BITS>
+__device__ inline f16x8 a_frag(const f16* lds, int tt, int s) {
+  const int l = threadIdx.x & 63, g = l >> 4;
+  const int col = BITS == 16 ? 32 * s + 8 * g : 32 * g + 8 * s;
+  return *reinterpret_cast<const f16x8*>(lds + (tt * 16 + (l & 15)) * kLdsRow + col);
+}
+
+// Weight fragments of one 16-row tile of one matrix for one stage.
+template <int BITS> struct WFrag;
+
+template <> struct WFrag<16> {
+  u32x4 v[4];
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
+                              int64_t ld, int64_t k0) {
+    const int g = (threadIdx.x & 63) >> 4;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int64_t col = k0 + 32 * s + 8 * g;
+      v[s] = (ok && col < ld)
+                 ? __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.w[m] + row * ld + col)))
+                 : u32x4{0, 0, 0, 0};
+    }
+  }
+  __device__ inline f16x8 get(int s) const { return __builtin_bit_cast(f16x8, v[s]); }
+};
+
+template <> struct WFrag<4> {
+  u32x4 q;
+  f16 sc;
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
+                              int64_t ld, int64_t k0) {
+    const int g = (threadIdx.x & 63) >> 4;
+    const int64_t col = k0 + 32 * g;
+    if (ok && col < ld) {
+      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.q[m] + row * (ld / 2) + col / 2)));
+      sc = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
+    } else {
+      q = u32x4{0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u};  // q = 0
+      sc = (f16)0.0f;
+    }
+  }
+  // word with e0..e7 at bits 4j -> (e0,e4)(e1,e5)(e2,e6)(e3,e7), scaled
+  __device__ inline f16x8 get(int s) const {
+    const uint32_t w = s == 0 ? q.x : (s == 1 ? q.y : (s == 2 ? q.z : q.w));
+    const f16x2 bias = as_h2(0x64086408u);  // 1032 = 1024 + 8
+    const f16x2 s2 = {sc, sc};
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      o[k] = as_u32((as_h2(((w >> (4 * k)) & 0x000F000Fu) | 0x64006400u) - bias) * s2);
+    return pack8(o[0], o[1], o[2], o[3]);
+  }
+};
+
+template <> struct WFrag<2> {
+  u32x2 q;
+  f16 sc;
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
+                              int64_t ld, int64_t k0) {
+    const int g = (threadIdx.x & 63) >> 4;
+    const int64_t col = k0 + 32 * g;
+    if (ok && col < ld) {
+      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x2*>(ex.q[m] + row * (ld / 4) + col / 4)));
+      sc = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
+    } else {
+      q = u32x2{0xAAAAAAAAu, 0xAAAAAAAAu};  // q = 0
+      sc = (f16)0.0f;
+    }
+  }
+  // half-word s holds e0..e7 at bits 2j; move byte 1 to byte 2 so that the
+  // mask 0x00030003 pairs (e_k, e_{k+4})
+  __device__ inline f16x8 get(int s) const {
+    const uint32_t w = (s < 2 ? q.x : q.y) >> (16 * (s & 1));
+    const uint32_t v = (w & 0xFFu) | ((w & 0xFF00u) << 8);
+    const f16x2 bias = as_h2(0x64026402u);  // 1026 = 1024 + 2
+    const f16x2 s2 = {sc, sc};
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      o[k] = as_u32((as_h2(((v >> (2 * k)) & 0x00030003u) | 0x64006400u) - bias) * s2);
+    return pack8(o[0], o[1], o[2], o[3]);
+  }
+};
+
+// One pass (up to 128 tokens) of one group over NM matrices: acc[rt][tt][m]
+// accumulates tokens of tile tt against weight rows of tile rt.
+template <int BITS, int NM, int RT>
+__device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
+                          int64_t wrow0, int64_t n_rows, int64_t ld,
+                          const f16* act, int64_t act_ld, const int32_t* perm,
+                          int off, int j0, int n, int K, bool gather, f16* lds,
+                          f32x4 (&acc)[RT][kTokTiles][NM]) {
+  const int l = threadIdx.x & 63;
+  const int ntile = (n + 15) >> 4;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tt = 0; tt < kTokTiles; ++tt)
+#pragma unroll
+      for (int m = 0; m < NM; ++m) acc[rt][tt][m] = f32x4{0, 0, 0, 0};
+  for (int64_t k0 = 0; k0 < ld; k0 += kStageK) {
+    WFrag<BITS> w[RT][NM];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int64_t row = wrow0 + rt * 16 + (l & 15);
+#pragma unroll
+      for (int m = 0; m < NM; ++m) w[rt][m].load(ex, mats[m], row, row < n_rows, ld, k0);
+    }
+    __syncthreads();  // previous stage's LDS reads are done
+    stage_act<BITS != 16>(lds, act, act_ld, perm, off, j0, n, K, gather, k0);
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      f16x8 b[RT][NM];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int m = 0; m < NM; ++m) b[rt][m] = w[rt][m].get(s);
+#pragma unroll
+      for (int tt = 0; tt < kTokTiles; ++tt) {
+        if (tt < ntile) {
+          const f16x8 a = a_frag<BITS>(lds, tt, s);
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int m = 0; m < NM; ++m)
+              acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[rt][m], acc[rt][tt][m], 0, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+template <int BITS>
+__device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* perm,
+                         const f16* x, f16* h, int d, int f, int K, f16* lds) {
+  constexpr int RT = kUpRowsW / 16;
+  const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t wrow0 = (int64_t)blockIdx.y * kWaves * kUpRowsW + wave * kUpRowsW;
+  const int mats[2] = {0, 1};
+  for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
+    const int n = min(kPassTok, g.count - j0);
+    f32x4 acc[RT][kTokTiles][2];
+    gemm_pass<BITS, 2, RT>(ex, mats, wrow0, f, d, x, d, perm, g.offset, j0, n, K, true, lds, acc);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int64_t row = wrow0 + rt * 16 + (l & 15);
+#pragma unroll
+      for (int tt = 0; tt < kTokTiles; ++tt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int j = tt * 16 + 4 * (l >> 4) + i;
+          if (j < n && row < f) {
+            const float a = acc[rt][tt][0][i], b = acc[rt][tt][1][i];
+            h[(int64_t)(g.offset + j0 + j) * f + row] = (f16)(a / (1.0f + expf(-a)) * b);
+          }
+        }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void prefill_up_kernel(
+    const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
+    const int32_t* __restrict__ perm, const f16* __restrict__ x, f16* __restrict__ h,
+    int d, int f, int K) {
+  __shared__ f16 lds[kPassTok * kLdsRow];
+  if ((int)blockIdx.x >= wl->n_groups) return;
+  const Group g = wl->groups[blockIdx.x];
+  const ExpertEntry ex = table[g.expert];
+  if (g.bits == 16) up_group<16>(ex, g, perm, x, h, d, f, K, lds);
+  else if (g.bits == 4) up_group<4>(ex, g, perm, x, h, d, f, K, lds);
+  else up_group<2>(ex, g, perm, x, h, d, f, K, lds);
+}
+
+template <int BITS>
+__device__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
+                           float* e, int d, int f, f16* lds) {
+  constexpr int RT = kDownRowsW / 16;
+  const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t wrow0 = (int64_t)blockIdx.y * kWaves * kDownRowsW + wave * kDownRowsW;
+  const int mats[1] = {2};
+  for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
+    const int n = min(kPassTok, g.count - j0);
+    f32x4 acc[RT][kTokTiles][1];
+    gemm_pass<BITS, 1, RT>(ex, mats, wrow0, d, f, h, f, nullptr, g.offset, j0, n, 1, false, lds, acc);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int64_t row = wrow0 + rt * 16 + (l & 15);
+#pragma unroll
+      for (int tt = 0; tt < kTokTiles; ++tt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int j = tt * 16 + 4 * (l >> 4) + i;
+          if (j < n && row < d) e[(int64_t)(g.offset + j0 + j) * d + row] = acc[rt][tt][0][i];
+        }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void prefill_down_kernel(
+    const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
+    const f16* __restrict__ h, float* __restrict__ e, int d, int f) {
+  __shared__ f16 lds[kPassTok * kLdsRow];
+  if ((int)blockIdx.x >= wl->n_groups) return;
+  const Group g = wl->groups[blockIdx.x];
+  const ExpertEntry ex = table[g.expert];
+  if (g.bits == 16) down_group<16>(ex, g, h, e, d, f, lds);
+  else if (g.bits == 4) down_group<4>(ex, g, h, e, d, f, lds);
+  else down_group<2>(ex, g, h, e, d, f, lds);
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// y[t] = sum_k w[t,k] * E[pos(t,k)] in slot order (skip -> 0); with h_res:
+// h_res[t] += that and x_next[t] = fp16(rmsnorm(h_res[t])).
+__global__ __launch_bounds__(kThreads) void combine_prefill_kernel(
+    const float* __restrict__ e, const int32_t* __restrict__ pos,
+    const float* __restrict__ w, const int8_t* __restrict__ prec, int d, int K,
+    float* __restrict__ y, float* __restrict__ h_res, f16* __restrict__ x_next,
+    float eps) {
+  __shared__ float red[kWaves];
+  __shared__ int s_pos[kMaxTopK];
+  __shared__ float s_w[kMaxTopK];
+  const int t = blockIdx.x;
+  if (threadIdx.x < K) {
+    const int p = t * K + threadIdx.x;
+    s_pos[threadIdx.x] = prec[p] == PREC_SKIP ? -1 : pos[p];
+    s_w[threadIdx.x] = w[p];
+  }
+  __syncthreads();
+  const int64_t base = (int64_t)t * d;
+  float ss = 0.0f;
+  for (int c = threadIdx.x; c < d; c += kThreads) {
+    float acc = 0.0f;
+    for (int k = 0; k < K; ++k)
+      if (s_pos[k] >= 0) acc = fmaf(s_w[k], e[(int64_t)s_pos[k] * d + c], acc);
+    if (h_res) {
+      const float v = h_res[base + c] + acc;
+      h_res[base + c] = v;
+      ss = fmaf(v, v, ss);
+    } else {
+      y[base + c] = acc;
+    }
+  }
+  if (!h_res) return;
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) tot += red[i];
+  const float r = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x; c < d; c += kThreads) x_next[base + c] = (f16)(h_res[base + c] * r);
+}
+
+}  // namespace
+
+hipError_t launch_prefill_up(const ExpertEntry* table, const WorkList* wl,
+                             const int32_t* perm, const f16* x, f16* h, int T,
+                             int d, int f, int K, int max_groups, hipStream_t s) {
+  (void)T;
+  const int rows_per_block = kWaves * kUpRowsW;
+  dim3 grid(max_groups, (f + rows_per_block - 1) / rows_per_block);
+  prefill_up_kernel<<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_down(const ExpertEntry* table, const WorkList* wl,
+                               const f16* h, float* e, int T, int d, int f, int K,
+                               int max_groups, hipStream_t s) {
+  (void)T;
+  (void)K;
+  const int rows_per_block = kWaves * kDownRowsW;
+  dim3 grid(max_groups, (d + rows_per_block - 1) / rows_per_block);
+  prefill_down_kernel<<<grid, kThreads, 0, s>>>(table, wl, h, e, d, f);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_prefill(const float* e, const int32_t* pos, const float* w,
+                                  const int8_t* prec, int T, int d, int K, float* y,
+                                  float* h_res, f16* x_next, float eps, hipStream_t s) {
+  combine_prefill_kernel<<<T, kThreads, 0, s>>>(e, pos, w, prec, d, K, y, h_res, x_next, eps);
+  return hipGetLastError();
 }
 
 }  // namespace moe
