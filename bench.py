@@ -204,6 +204,106 @@ def run_decode_layer(args):
     return out, (wl, tags, xs, y, idx, gw, prec, layers)
 
 
+def stack_bytes_flops(wl, idx, prec, tags_per_layer):
+    """Algorithmic bytes (distinct expert copies + gates) and FLOPs of one pass
+    over the stack, from the routing each layer chose."""
+    d, f = wl.d_model, wl.d_ff
+    b = fl = 0
+    for l in range(wl.n_layers):
+        b += step_bytes(wl, idx[l], prec[l], tags_per_layer[l])[0]
+        fl += int((prec[l] != 2).sum()) * 2 * 3 * d * f
+    return b, fl
+
+
+def run_stack(args):
+    """32-layer stacks (residual glue between layers): the Phi-MoE-shaped
+    decode stack (4 tokens) or the Mixtral-shaped prefill stack (512)."""
+    import torch
+    import gpu_support as S
+    from oracle import moe_oracle as O
+    from synth import configs as C
+
+    wl = C.BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    T, K, d, NL = wl.n_tokens, wl.top_k, wl.d_model, wl.n_layers
+    log(f"workload {wl.name}: generating {NL} layers in HBM")
+    layers, keep, tags_l = [], [], []
+    for l in range(NL):
+        tags = C.layer_tags(wl, l)
+        w = S.device_layer_weights(wl, l, device=dev)
+        keep.append(w)
+        tags_l.append(tags)
+        layers.append(S.make_layer(wl, tags, w, max_tokens=T))
+    h0_np = C.hidden_states(wl).astype(np.float32)
+    x0_np = O.rmsnorm(h0_np.astype(np.float64)).astype(np.float16)
+    h0 = torch.from_numpy(h0_np).to(dev)
+    h = torch.empty_like(h0)
+    xb = [torch.from_numpy(x0_np).to(dev), torch.empty((T, d), dtype=torch.float16, device=dev)]
+    x_first = xb[0].clone()
+    idx = torch.empty((NL, T, K), dtype=torch.int32, device=dev)
+    gw = torch.empty((NL, T, K), dtype=torch.float32, device=dev)
+    prec = torch.empty((NL, T, K), dtype=torch.int8, device=dev)
+    prefill = wl.mode == "prefill"
+
+    def step():
+        h.copy_(h0)
+        xb[0].copy_(x_first)
+        for l, L in enumerate(layers):
+            xi, xo = xb[l % 2], xb[(l + 1) % 2]
+            if prefill:
+                L.prefill_residual(xi, h, xo, idx[l], gw[l], prec[l])
+            else:
+                L.decode_step_residual(xi, h, xo, idx[l], gw[l], prec[l])
+
+    log("warmup", args.warmup)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log("timing", args.steps, "steps")
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    b, fl = stack_bytes_flops(wl, idx.cpu().numpy(), prec.cpu().numpy(), tags_l)
+
+    log("stage timing pass")
+    for L in layers:
+        L.enable_timing(True)
+    for _ in range(max(2, args.steps // 2)):
+        step()
+    torch.cuda.synchronize()
+    tot = np.zeros(4)
+    calls = 0
+    for L in layers:
+        t, n = L.stage_times()
+        tot += np.array(t)
+        calls += n
+        L.enable_timing(False)
+    stage_us = (tot / max(calls, 1) * 1e3).tolist()
+    t_s = ms * 1e-3
+    frac = max(b / 8e12, fl / 2.5e15) / t_s
+    out = {
+        "metric": METRIC, "value": T / t_s, "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+        "config": {"workload": wl.name, "d_model": d, "d_ff": wl.d_ff,
+                   "n_experts": wl.n_experts, "top_k": K, "tokens_per_step": T,
+                   "layers": NL, "mode": wl.mode, "tags": wl.note},
+        "effective_weight_GBps": b / t_s / 1e9,
+        "pct_hbm_peak": 100.0 * b / t_s / 1e9 / HBM_PEAK_GBPS,
+        "bytes_per_step": b, "flops_per_step": fl,
+        "mfma_util": fl / t_s / 2.5e15 if prefill else None,
+        "roofline_step": {"bound": "hbm" if b / 8e12 >= fl / 2.5e15 else "mfma",
+                          "frac": frac},
+        "stage_us_per_layer": dict(zip(["route", "up", "down", "rmsnorm"], stage_us)),
+    }
+    return out
+
+
 def parity_and_cpu(args, state, out):
     """Check sampled steps against the oracle and time the oracle itself."""
     import torch
@@ -284,6 +384,11 @@ def main():
     torch.cuda.set_device(0)
     import paper_2411_01433_amd as P
     P.lib()
+    from synth import configs as C
+    if C.BY_NAME[args.workload].n_layers > 1:
+        out = run_stack(args)
+        print(json.dumps(out), flush=True)
+        return
     out, state = run_decode_layer(args)
     if not args.no_cpu_baseline:
         parity_and_cpu(args, state, out)

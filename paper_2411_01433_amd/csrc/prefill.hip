@@ -14,16 +14,20 @@
 //
 // Tiling (v_mfma_f32_16x16x32_f16: lane l holds A[l%16][8(l/16)+i],
 // B[8(l/16)+i][l%16] and C[4(l/16)+i][l%16]): M = tokens (A = activations
-// from LDS, up to 128 per pass = 8 tiles), N = weight rows (B = weight
+// from LDS, up to 192 per pass = 12 tiles), N = weight rows (B = weight
 // rows, each lane's 8 k-values contiguous in memory), K = reduction dim in
-// stages of 128.  A block of 4 waves owns 4 x ROWS_W weight rows; each wave
-// owns ROWS_W rows for all the pass's tokens, so every weight element is
-// fetched from HBM once per pass and used 128 times.  Weight fragments are
+// stages of 64.  A block of 8 waves owns 8 x 16 weight rows; each wave owns
+// 16 rows for all the pass's tokens (up to 192), so every weight element is
+// fetched from HBM once per pass and used by every token of the group, and
+// each staged activation tile serves 128 weight rows.  Activations are
+// double-buffered in LDS (one barrier per stage, the next stage fetched
+// into registers during the MFMAs) and weight fragments are loaded two
+// stages ahead.  Weight fragments are
 // loaded straight into registers with nontemporal loads:
 //   fp16: lane group g (= l/16) reads 16 B at k = 32s + 8g for step s;
-//   int4: lane group g reads the whole 16 B group g of the stage (32 codes)
-//         and step s uses its word s;
-//   int2: lane group g reads the 8 B group g and step s uses half-word s;
+//   int4: lane group g reads the 8 B half group of columns 16g..16g+15 of
+//         the stage and step s uses its word s;
+//   int2: lane group g reads the 4 B of the same columns, half-word s;
 // low codes are turned into fp16 with the 0x6400|u == 1024+u trick and
 // scaled by the group's fp16 scale (w = fp16(q*s)); the pair order this
 // produces, (e0,e4)(e1,e5)(e2,e6)(e3,e7), is matched by staging the
@@ -34,14 +38,18 @@ namespace moe {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
-constexpr int kStageK = 128;              // reduction columns per stage
-constexpr int kPassTok = 128;             // tokens per pass (8 MFMA tiles)
+constexpr int kThreads = 512;
+constexpr int kWaves = 8;
+constexpr int kStageK = 64;               // reduction columns per stage (2 MFMA steps)
+constexpr int kSteps = kStageK / 32;
+constexpr int kPassTok = 192;             // tokens per pass (12 MFMA tiles)
 constexpr int kTokTiles = kPassTok / 16;
 constexpr int kLdsRow = kStageK + 8;      // halves per staged row (16 B pad)
-constexpr int kUpRowsW = 32;              // weight rows per wave, up-projection
+constexpr int kUpRowsW = 16;              // weight rows per wave, up-projection
 constexpr int kDownRowsW = 16;            // weight rows per wave, down-projection
+// staging: thread t owns rows (t >> 3) + 32 i of the pass and 8-column piece t & 7
+constexpr int kPieces = kStageK / 8;
+constexpr int kStageRowsPerThread = kPassTok / (kThreads / kPieces);
 
 typedef __attribute__((address_space(1))) const u32x4* gvec4;
 
@@ -61,37 +69,58 @@ __device__ inline f16x8 pack8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
 // low-precision groups: x0 x4 x1 x5 x2 x6 x3 x7.
 __device__ inline int perm8(int i) { return i < 4 ? 2 * i : 2 * (i - 4) + 1; }
 
-// Stage rows [j0, j0 + n) of the group's activation matrix, columns
-// [k0, k0 + 128), into LDS [128][kLdsRow]; rows beyond n and columns beyond
-// ld are zero.  Source row of group row j: perm[off + j] / K (token rows of
-// x) or off + j (rows of H, already in group order).
-template <bool PERMUTE>
-__device__ void stage_act(f16* lds, const f16* src, int64_t ld, const int32_t* perm,
-                          int off, int j0, int n, int K, bool gather, int64_t k0) {
-  for (int e = threadIdx.x; e < kPassTok * (kStageK / 8); e += kThreads) {
-    const int r = e >> 4, piece = e & 15;
-    const int64_t col = k0 + piece * 8;
-    u32x4 v = {0, 0, 0, 0};
-    if (r < n && col < ld) {
-      const int64_t row = gather ? perm[off + j0 + r] / K : (int64_t)(off + j0 + r);
-      v = *reinterpret_cast<const u32x4*>(src + row * ld + col);
-    }
-    if (PERMUTE) {
-      const f16x8 a = __builtin_bit_cast(f16x8, v);
-      f16x8 b;
+// Activation staging of one pass.  Thread t owns rows (t >> 3) + 32 i of
+// the pass and the 8-column piece t & 7 of every stage; the source rows
+// are resolved once per pass (group row j is token perm[off + j] / K of x,
+// or row off + j of H which is already in group order), then each stage
+// is fetched into registers one stage ahead and written to LDS [row][k]
+// (rows beyond n and columns beyond ld are zero).
+struct ActStager {
+  const f16* row[kStageRowsPerThread];
+  u32x4 v[kStageRowsPerThread];
+
+  __device__ void init(const f16* src, int64_t ld, const int32_t* perm, int off,
+                       int j0, int n, int K, bool gather) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) b[perm8(i)] = a[i];
-      v = __builtin_bit_cast(u32x4, b);
+    for (int i = 0; i < kStageRowsPerThread; ++i) {
+      const int r = (threadIdx.x / kPieces) + (kThreads / kPieces) * i;
+      row[i] = nullptr;
+      if (r < n) {
+        const int64_t sr = gather ? perm[off + j0 + r] / K : (int64_t)(off + j0 + r);
+        row[i] = src + sr * ld;
+      }
     }
-    *reinterpret_cast<u32x4*>(lds + r * kLdsRow + piece * 8) = v;
   }
-}
+  __device__ void fetch(int64_t ld, int64_t k0) {
+    const int64_t col = k0 + (threadIdx.x % kPieces) * 8;
+#pragma unroll
+    for (int i = 0; i < kStageRowsPerThread; ++i)
+      v[i] = (row[i] && col < ld) ? *reinterpret_cast<const u32x4*>(row[i] + col)
+                                  : u32x4{0, 0, 0, 0};
+  }
+  template <bool PERMUTE>
+  __device__ void store(f16* lds) const {
+#pragma unroll
+    for (int i = 0; i < kStageRowsPerThread; ++i) {
+      u32x4 x = v[i];
+      if (PERMUTE) {
+        const f16x8 a = __builtin_bit_cast(f16x8, x);
+        f16x8 b;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) b[perm8(e)] = a[e];
+        x = __builtin_bit_cast(u32x4, b);
+      }
+      const int r = (threadIdx.x / kPieces) + (kThreads / kPieces) * i;
+      *reinterpret_cast<u32x4*>(lds + r * kLdsRow + (threadIdx.x % kPieces) * 8) = x;
+    }
+  }
+};
 
 // A fragment (activations) of token tile tt for step s of the stage.
 template <int BITS>
 __device__ inline f16x8 a_frag(const f16* lds, int tt, int s) {
   const int l = threadIdx.x & 63, g = l >> 4;
-  const int col = BITS == 16 ? 32 * s + 8 * g : 32 * g + 8 * s;
+  const int col = BITS == 16 ? 32 * s + 8 * g : 16 * g + 8 * s;
   return *reinterpret_cast<const f16x8*>(lds + (tt * 16 + (l & 15)) * kLdsRow + col);
 }
 
@@ -99,12 +128,12 @@ __device__ inline f16x8 a_frag(const f16* lds, int tt, int s) {
 template <int BITS> struct WFrag;
 
 template <> struct WFrag<16> {
-  u32x4 v[4];
+  u32x4 v[kSteps];
   __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
                               int64_t ld, int64_t k0) {
     const int g = (threadIdx.x & 63) >> 4;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < kSteps; ++s) {
       const int64_t col = k0 + 32 * s + 8 * g;
       v[s] = (ok && col < ld)
                  ? __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.w[m] + row * ld + col)))
@@ -115,23 +144,24 @@ template <> struct WFrag<16> {
 };
 
 template <> struct WFrag<4> {
-  u32x4 q;
+  u32x2 q;
   f16 sc;
+  // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
   __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
                               int64_t ld, int64_t k0) {
     const int g = (threadIdx.x & 63) >> 4;
-    const int64_t col = k0 + 32 * g;
+    const int64_t col = k0 + 16 * g;
     if (ok && col < ld) {
-      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.q[m] + row * (ld / 2) + col / 2)));
+      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x2*>(ex.q[m] + row * (ld / 2) + col / 2)));
       sc = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
     } else {
-      q = u32x4{0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u};  // q = 0
+      q = u32x2{0x88888888u, 0x88888888u};  // q = 0
       sc = (f16)0.0f;
     }
   }
   // word with e0..e7 at bits 4j -> (e0,e4)(e1,e5)(e2,e6)(e3,e7), scaled
   __device__ inline f16x8 get(int s) const {
-    const uint32_t w = s == 0 ? q.x : (s == 1 ? q.y : (s == 2 ? q.z : q.w));
+    const uint32_t w = s == 0 ? q.x : q.y;
     const f16x2 bias = as_h2(0x64086408u);  // 1032 = 1024 + 8
     const f16x2 s2 = {sc, sc};
     uint32_t o[4];
@@ -143,24 +173,25 @@ template <> struct WFrag<4> {
 };
 
 template <> struct WFrag<2> {
-  u32x2 q;
+  uint32_t q;
   f16 sc;
+  // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
   __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
                               int64_t ld, int64_t k0) {
     const int g = (threadIdx.x & 63) >> 4;
-    const int64_t col = k0 + 32 * g;
+    const int64_t col = k0 + 16 * g;
     if (ok && col < ld) {
-      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x2*>(ex.q[m] + row * (ld / 4) + col / 4)));
+      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const uint32_t*>(ex.q[m] + row * (ld / 4) + col / 4)));
       sc = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
     } else {
-      q = u32x2{0xAAAAAAAAu, 0xAAAAAAAAu};  // q = 0
+      q = 0xAAAAAAAAu;  // q = 0
       sc = (f16)0.0f;
     }
   }
   // half-word s holds e0..e7 at bits 2j; move byte 1 to byte 2 so that the
   // mask 0x00030003 pairs (e_k, e_{k+4})
   __device__ inline f16x8 get(int s) const {
-    const uint32_t w = (s < 2 ? q.x : q.y) >> (16 * (s & 1));
+    const uint32_t w = q >> (16 * s);
     const uint32_t v = (w & 0xFFu) | ((w & 0xFF00u) << 8);
     const f16x2 bias = as_h2(0x64026402u);  // 1026 = 1024 + 2
     const f16x2 s2 = {sc, sc};
@@ -172,8 +203,10 @@ template <> struct WFrag<2> {
   }
 };
 
-// One pass (up to 128 tokens) of one group over NM matrices: acc[rt][tt][m]
-// accumulates tokens of tile tt against weight rows of tile rt.
+// One pass (up to kPassTok tokens) of one group over NM matrices:
+// acc[rt][tt][m] accumulates the tokens of tile tt against the weight rows
+// of tile rt.  Software pipeline: while the MFMAs of stage k run, the
+// activations and weight fragments of stage k+1 are already in flight.
 template <int BITS, int NM, int RT>
 __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
                           int64_t wrow0, int64_t n_rows, int64_t ld,
@@ -188,28 +221,41 @@ __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
     for (int tt = 0; tt < kTokTiles; ++tt)
 #pragma unroll
       for (int m = 0; m < NM; ++m) acc[rt][tt][m] = f32x4{0, 0, 0, 0};
-  for (int64_t k0 = 0; k0 < ld; k0 += kStageK) {
-    WFrag<BITS> w[RT][NM];
+  auto load_w = [&](WFrag<BITS> (&w)[RT][NM], int64_t k0) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int64_t row = wrow0 + rt * 16 + (l & 15);
 #pragma unroll
       for (int m = 0; m < NM; ++m) w[rt][m].load(ex, mats[m], row, row < n_rows, ld, k0);
     }
-    __syncthreads();  // previous stage's LDS reads are done
-    stage_act<BITS != 16>(lds, act, act_ld, perm, off, j0, n, K, gather, k0);
+  };
+  ActStager st;
+  st.init(act, act_ld, perm, off, j0, n, K, gather);
+  st.fetch(act_ld, 0);
+  WFrag<BITS> w0[RT][NM], w1[RT][NM];
+  load_w(w0, 0);
+  load_w(w1, kStageK);   // masked beyond ld
+  int buf = 0;
+  for (int64_t k0 = 0; k0 < ld; k0 += kStageK, buf ^= 1) {
+    f16* cur = lds + buf * (kPassTok * kLdsRow);
+    // the buffer written here was last read two stages ago, before the
+    // previous stage's barrier
+    st.store<BITS != 16>(cur);
     __syncthreads();
+    if (k0 + kStageK < ld) st.fetch(act_ld, k0 + kStageK);
+    WFrag<BITS> w2[RT][NM];
+    load_w(w2, k0 + 2 * kStageK);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < kSteps; ++s) {
       f16x8 b[RT][NM];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int m = 0; m < NM; ++m) b[rt][m] = w[rt][m].get(s);
+        for (int m = 0; m < NM; ++m) b[rt][m] = w0[rt][m].get(s);
 #pragma unroll
       for (int tt = 0; tt < kTokTiles; ++tt) {
         if (tt < ntile) {
-          const f16x8 a = a_frag<BITS>(lds, tt, s);
+          const f16x8 a = a_frag<BITS>(cur, tt, s);
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -218,7 +264,15 @@ __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
         }
       }
     }
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        w0[rt][m] = w1[rt][m];
+        w1[rt][m] = w2[rt][m];
+      }
   }
+  __syncthreads();  // the LDS buffers are reused by the next pass
 }
 
 template <int BITS>
@@ -253,7 +307,7 @@ __global__ __launch_bounds__(kThreads) void prefill_up_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
     const int32_t* __restrict__ perm, const f16* __restrict__ x, f16* __restrict__ h,
     int d, int f, int K) {
-  __shared__ f16 lds[kPassTok * kLdsRow];
+  __shared__ f16 lds[2 * kPassTok * kLdsRow];
   if ((int)blockIdx.x >= wl->n_groups) return;
   const Group g = wl->groups[blockIdx.x];
   const ExpertEntry ex = table[g.expert];
@@ -290,7 +344,7 @@ __device__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
 __global__ __launch_bounds__(kThreads) void prefill_down_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
     const f16* __restrict__ h, float* __restrict__ e, int d, int f) {
-  __shared__ f16 lds[kPassTok * kLdsRow];
+  __shared__ f16 lds[2 * kPassTok * kLdsRow];
   if ((int)blockIdx.x >= wl->n_groups) return;
   const Group g = wl->groups[blockIdx.x];
   const ExpertEntry ex = table[g.expert];
