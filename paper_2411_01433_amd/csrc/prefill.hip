@@ -22,16 +22,18 @@
 // each staged activation tile serves 128 weight rows.  Activations are
 // double-buffered in LDS (one barrier per stage, the next stage fetched
 // into registers during the MFMAs) and weight fragments are loaded two
-// stages ahead.  Weight fragments are
-// loaded straight into registers with nontemporal loads:
+// stages ahead, straight into registers:
 //   fp16: lane group g (= l/16) reads 16 B at k = 32s + 8g for step s;
 //   int4: lane group g reads the 8 B half group of columns 16g..16g+15 of
 //         the stage and step s uses its word s;
-//   int2: lane group g reads the 4 B of the same columns, half-word s;
-// low codes are turned into fp16 with the 0x6400|u == 1024+u trick and
-// scaled by the group's fp16 scale (w = fp16(q*s)); the pair order this
-// produces, (e0,e4)(e1,e5)(e2,e6)(e3,e7), is matched by staging the
-// activations in LDS with the same permutation inside every 8 elements.
+//   int2: lane group g reads the 4 B of the same columns, half-word s.
+// One load instruction covers 64 of each row's 128 stage bytes, so weight
+// loads are plain (the line stays in L2 for the other half; nontemporal
+// loads measured 20% more HBM traffic here).  Low codes are turned into
+// fp16 with the 0x6400|u == 1024+u trick and scaled by the group's fp16
+// scale (w = fp16(q*s)); the pair order this produces,
+// (e0,e4)(e1,e5)(e2,e6)(e3,e7), is matched by staging the activations in
+// LDS with the same permutation inside every 8 elements.
 #include "moe_internal.h"
 
 namespace moe {
@@ -136,7 +138,7 @@ template <> struct WFrag<16> {
     for (int s = 0; s < kSteps; ++s) {
       const int64_t col = k0 + 32 * s + 8 * g;
       v[s] = (ok && col < ld)
-                 ? __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.w[m] + row * ld + col)))
+                 ? *gmem(reinterpret_cast<const u32x4*>(ex.w[m] + row * ld + col))
                  : u32x4{0, 0, 0, 0};
     }
   }
@@ -152,8 +154,8 @@ template <> struct WFrag<4> {
     const int g = (threadIdx.x & 63) >> 4;
     const int64_t col = k0 + 16 * g;
     if (ok && col < ld) {
-      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x2*>(ex.q[m] + row * (ld / 2) + col / 2)));
-      sc = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
+      q = *gmem(reinterpret_cast<const u32x2*>(ex.q[m] + row * (ld / 2) + col / 2));
+      sc = *gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup);
     } else {
       q = u32x2{0x88888888u, 0x88888888u};  // q = 0
       sc = (f16)0.0f;
@@ -181,8 +183,8 @@ template <> struct WFrag<2> {
     const int g = (threadIdx.x & 63) >> 4;
     const int64_t col = k0 + 16 * g;
     if (ok && col < ld) {
-      q = __builtin_nontemporal_load(gmem(reinterpret_cast<const uint32_t*>(ex.q[m] + row * (ld / 4) + col / 4)));
-      sc = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
+      q = *gmem(reinterpret_cast<const uint32_t*>(ex.q[m] + row * (ld / 4) + col / 4));
+      sc = *gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup);
     } else {
       q = 0xAAAAAAAAu;  // q = 0
       sc = (f16)0.0f;
@@ -277,10 +279,10 @@ __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
 
 template <int BITS>
 __device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* perm,
-                         const f16* x, f16* h, int d, int f, int K, f16* lds) {
+                         const f16* x, f16* h, int d, int f, int K, int tile, f16* lds) {
   constexpr int RT = kUpRowsW / 16;
   const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t wrow0 = (int64_t)blockIdx.y * kWaves * kUpRowsW + wave * kUpRowsW;
+  const int64_t wrow0 = (int64_t)tile * kWaves * kUpRowsW + wave * kUpRowsW;
   const int mats[2] = {0, 1};
   for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
     const int n = min(kPassTok, g.count - j0);
@@ -303,25 +305,32 @@ __device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* p
   }
 }
 
+// Blocks are numbered group-major (all row tiles of work group 0, then of
+// group 1, ...): the hardware hands consecutive blocks to the 8 XCDs in
+// turn, so each group's tiles are spread over every XCD (balanced bytes per
+// XCD whatever the group's precision) and the tiles of one group, which
+// read the same activation columns at about the same time, share them in
+// each XCD's L2.
 __global__ __launch_bounds__(kThreads) void prefill_up_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
     const int32_t* __restrict__ perm, const f16* __restrict__ x, f16* __restrict__ h,
-    int d, int f, int K) {
+    int d, int f, int K, int n_tiles) {
   __shared__ f16 lds[2 * kPassTok * kLdsRow];
-  if ((int)blockIdx.x >= wl->n_groups) return;
-  const Group g = wl->groups[blockIdx.x];
+  const int gi = blockIdx.x / n_tiles, tile = blockIdx.x - gi * n_tiles;
+  if (gi >= wl->n_groups) return;
+  const Group g = wl->groups[gi];
   const ExpertEntry ex = table[g.expert];
-  if (g.bits == 16) up_group<16>(ex, g, perm, x, h, d, f, K, lds);
-  else if (g.bits == 4) up_group<4>(ex, g, perm, x, h, d, f, K, lds);
-  else up_group<2>(ex, g, perm, x, h, d, f, K, lds);
+  if (g.bits == 16) up_group<16>(ex, g, perm, x, h, d, f, K, tile, lds);
+  else if (g.bits == 4) up_group<4>(ex, g, perm, x, h, d, f, K, tile, lds);
+  else up_group<2>(ex, g, perm, x, h, d, f, K, tile, lds);
 }
 
 template <int BITS>
 __device__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
-                           float* e, int d, int f, f16* lds) {
+                           float* e, int d, int f, int tile, f16* lds) {
   constexpr int RT = kDownRowsW / 16;
   const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t wrow0 = (int64_t)blockIdx.y * kWaves * kDownRowsW + wave * kDownRowsW;
+  const int64_t wrow0 = (int64_t)tile * kWaves * kDownRowsW + wave * kDownRowsW;
   const int mats[1] = {2};
   for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
     const int n = min(kPassTok, g.count - j0);
@@ -343,14 +352,15 @@ __device__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
 
 __global__ __launch_bounds__(kThreads) void prefill_down_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
-    const f16* __restrict__ h, float* __restrict__ e, int d, int f) {
+    const f16* __restrict__ h, float* __restrict__ e, int d, int f, int n_tiles) {
   __shared__ f16 lds[2 * kPassTok * kLdsRow];
-  if ((int)blockIdx.x >= wl->n_groups) return;
-  const Group g = wl->groups[blockIdx.x];
+  const int gi = blockIdx.x / n_tiles, tile = blockIdx.x - gi * n_tiles;
+  if (gi >= wl->n_groups) return;
+  const Group g = wl->groups[gi];
   const ExpertEntry ex = table[g.expert];
-  if (g.bits == 16) down_group<16>(ex, g, h, e, d, f, lds);
-  else if (g.bits == 4) down_group<4>(ex, g, h, e, d, f, lds);
-  else down_group<2>(ex, g, h, e, d, f, lds);
+  if (g.bits == 16) down_group<16>(ex, g, h, e, d, f, tile, lds);
+  else if (g.bits == 4) down_group<4>(ex, g, h, e, d, f, tile, lds);
+  else down_group<2>(ex, g, h, e, d, f, tile, lds);
 }
 
 __device__ inline float wave_sum(float v) {
@@ -408,8 +418,8 @@ hipError_t launch_prefill_up(const ExpertEntry* table, const WorkList* wl,
                              int d, int f, int K, int max_groups, hipStream_t s) {
   (void)T;
   const int rows_per_block = kWaves * kUpRowsW;
-  dim3 grid(max_groups, (f + rows_per_block - 1) / rows_per_block);
-  prefill_up_kernel<<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K);
+  const int n_tiles = (f + rows_per_block - 1) / rows_per_block;
+  prefill_up_kernel<<<max_groups * n_tiles, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K, n_tiles);
   return hipGetLastError();
 }
 
@@ -419,8 +429,8 @@ hipError_t launch_prefill_down(const ExpertEntry* table, const WorkList* wl,
   (void)T;
   (void)K;
   const int rows_per_block = kWaves * kDownRowsW;
-  dim3 grid(max_groups, (d + rows_per_block - 1) / rows_per_block);
-  prefill_down_kernel<<<grid, kThreads, 0, s>>>(table, wl, h, e, d, f);
+  const int n_tiles = (d + rows_per_block - 1) / rows_per_block;
+  prefill_down_kernel<<<max_groups * n_tiles, kThreads, 0, s>>>(table, wl, h, e, d, f, n_tiles);
   return hipGetLastError();
 }
 
