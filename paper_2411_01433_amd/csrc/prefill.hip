@@ -370,7 +370,8 @@ __device__ inline float wave_sum(float v) {
 }
 
 // y[t] = sum_k w[t,k] * E[pos(t,k)] in slot order (skip -> 0); with h_res:
-// h_res[t] += that and x_next[t] = fp16(rmsnorm(h_res[t])).
+// h_res[t] += that and x_next[t] = fp16(rmsnorm(h_res[t])).  One block per
+// token, 4 columns per thread per step (d is a multiple of 64).
 __global__ __launch_bounds__(kThreads) void combine_prefill_kernel(
     const float* __restrict__ e, const int32_t* __restrict__ pos,
     const float* __restrict__ w, const int8_t* __restrict__ prec, int d, int K,
@@ -388,16 +389,19 @@ __global__ __launch_bounds__(kThreads) void combine_prefill_kernel(
   __syncthreads();
   const int64_t base = (int64_t)t * d;
   float ss = 0.0f;
-  for (int c = threadIdx.x; c < d; c += kThreads) {
-    float acc = 0.0f;
+  for (int c = threadIdx.x * 4; c < d; c += kThreads * 4) {
+    f32x4 acc = {0, 0, 0, 0};
     for (int k = 0; k < K; ++k)
-      if (s_pos[k] >= 0) acc = fmaf(s_w[k], e[(int64_t)s_pos[k] * d + c], acc);
+      if (s_pos[k] >= 0) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(e + (int64_t)s_pos[k] * d + c);
+        acc += s_w[k] * v;
+      }
     if (h_res) {
-      const float v = h_res[base + c] + acc;
-      h_res[base + c] = v;
-      ss = fmaf(v, v, ss);
+      f32x4 hv = *reinterpret_cast<const f32x4*>(h_res + base + c) + acc;
+      *reinterpret_cast<f32x4*>(h_res + base + c) = hv;
+      ss += hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
     } else {
-      y[base + c] = acc;
+      *reinterpret_cast<f32x4*>(y + base + c) = acc;
     }
   }
   if (!h_res) return;
@@ -408,7 +412,12 @@ __global__ __launch_bounds__(kThreads) void combine_prefill_kernel(
 #pragma unroll
   for (int i = 0; i < kWaves; ++i) tot += red[i];
   const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += kThreads) x_next[base + c] = (f16)(h_res[base + c] * r);
+  for (int c = threadIdx.x * 4; c < d; c += kThreads * 4) {
+    const f32x4 hv = *reinterpret_cast<const f32x4*>(h_res + base + c);
+    f16x4 o;
+    o[0] = (f16)(hv.x * r); o[1] = (f16)(hv.y * r); o[2] = (f16)(hv.z * r); o[3] = (f16)(hv.w * r);
+    *reinterpret_cast<f16x4*>(x_next + base + c) = o;
+  }
 }
 
 }  // namespace

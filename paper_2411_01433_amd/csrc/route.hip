@@ -17,7 +17,7 @@ namespace moe {
 namespace {
 
 constexpr int kRouteThreads = 1024;
-constexpr int kPrefillTokPerBlock = 8;
+constexpr int kPrefillTokPerBlock = 1;
 constexpr int kPrefillThreads = 256;
 
 // fp16-pair dot product with fp32 accumulation.  The operands are taken
@@ -126,14 +126,20 @@ __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
 }
 
 // Stable counting sort of all T*K pairs by key = expert*2 + (low ? 1 : 0)
-// (skipped pairs get no key).  Run by one whole block.
+// (skipped pairs get no key).  Run by one whole block of kRouteThreads.
+// Pairs are taken one block-wide chunk at a time; inside a wave, lanes with
+// equal keys are found with one ballot per distinct key, and a lane's rank
+// among them is the number of lower lanes in that ballot; per-wave counts
+// are then scanned across waves, so pair order inside a group is the pair
+// index order.
 __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
                                const int8_t* prec, const int* low_bits,
                                WorkList* wl, int32_t* perm, int32_t* pos) {
+  constexpr int kW = kRouteThreads / 64;
   __shared__ int cnt[kMaxKeys];
   __shared__ int base[kMaxKeys];
-  __shared__ int chunk_keys[kRouteThreads];
-  const int tid = threadIdx.x;
+  __shared__ int wcnt[kW][kMaxKeys];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int N = p.T * p.K;
   const int n_keys = 2 * p.E;
   for (int k = tid; k < n_keys; k += blockDim.x) cnt[k] = 0;
@@ -164,28 +170,39 @@ __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
     wl->n_groups = ng;
     wl->max_count = mx;
   }
-  __syncthreads();
-  // placement, one chunk of blockDim pairs at a time
+  const uint64_t lower = (1ull << lane) - 1ull;
   for (int c0 = 0; c0 < N; c0 += blockDim.x) {
+    for (int v = tid; v < kW * n_keys; v += blockDim.x) wcnt[v / n_keys][v % n_keys] = 0;
+    __syncthreads();
     const int i = c0 + tid;
     int key = -1;
     if (i < N && prec[i] != PREC_SKIP) key = idx[i] * 2 + (prec[i] == PREC_LOW);
-    chunk_keys[tid] = key;
-    __syncthreads();
-    if (key >= 0) {
-      int r = 0;
-      for (int j = 0; j < tid; ++j) r += (chunk_keys[j] == key);
-      const int at = base[key] + r;
-      perm[at] = i;
-      pos[i] = at;
+    int rank = 0;
+    uint64_t todo = __ballot(key >= 0);
+    while (todo) {
+      const int leader = __ffsll((unsigned long long)todo) - 1;
+      const int k = __builtin_amdgcn_readlane(key, leader);
+      const uint64_t m = __ballot(key == k);
+      if (key == k) rank = __popcll(m & lower);
+      if (lane == leader) wcnt[wave][k] = __popcll(m);
+      todo &= ~m;
     }
     __syncthreads();
-    // advance bases by this chunk's counts
+    // exclusive scan of the per-wave counts, per key
     if (tid < n_keys) {
-      int add = 0;
-      const int n_in = min((int)blockDim.x, N - c0);
-      for (int j = 0; j < n_in; ++j) add += (chunk_keys[j] == tid);
-      base[tid] += add;
+      int run = base[tid];
+      for (int w = 0; w < kW; ++w) {
+        const int c = wcnt[w][tid];
+        wcnt[w][tid] = run;
+        run += c;
+      }
+      base[tid] = run;
+    }
+    __syncthreads();
+    if (key >= 0) {
+      const int at = wcnt[wave][key] + rank;
+      perm[at] = i;
+      pos[i] = at;
     }
     __syncthreads();
   }
