@@ -43,7 +43,7 @@ constexpr int kMaxChunkTokens = 8;  // tokens per register tile
 // T=1 step against 128 us with 8 rows and 132 us with 16; 2-row up tiles
 // with 4-row down tiles: 109 us).
 template <int NTMAX> struct UpRows { static constexpr int value = NTMAX <= 2 ? 2 : 4; };
-template <int NTMAX> struct DownRows { static constexpr int value = NTMAX <= 2 ? 4 : 4; };
+template <int NTMAX> struct DownRows { static constexpr int value = NTMAX <= 2 ? 4 : 8; };
 
 // Scalar-argument casts on purpose: clang's __builtin_bit_cast applied
 // directly to a vector component expression (v.y) reads component 0.

@@ -1,0 +1,398 @@
+// Decode-path expert kernels on the matrix cores, for steps with several
+// tokens per expert copy.  Same mathematics as decode.hip:
+//
+//   up:    h[p, r] = silu(W1[r,:] . x_t) * (W3[r,:] . x_t)          (fp16)
+//   down:  e[q, r] = W2[r,:] . h[p]   for the pair p at work-list slot q
+//          (fp32; the combine kernel forms sum_k w[t,k] e[pos(t,k), :])
+//
+// With several tokens per weight row the dot2 kernels spend more VALU issue
+// per streamed byte than the HBM stream leaves (int4: dequantise plus one
+// dot2 per token per weight pair).  Here one v_mfma_f32_16x16x32_f16 takes
+// 16 weight rows x 32 columns (B operand, dequantised once) against up to
+// 16 tokens (A operand), so the per-token cost moves to the matrix cores.
+// MFMA lane layout: A[l%16][8(l/16)+i], B[8(l/16)+i][l%16], C[4(l/16)+i][l%16].
+//
+// Weight streaming.  A block owns 16 rows of one or two matrices; its waves
+// take turns along the reduction dimension in stages of 128 bytes per row (64 fp16 columns, 256
+// int4 or 512 int2 codes).  Each of the two 16-byte loads of a stage covers
+// 8 rows x one full 128-byte line: lane l reads chunk l/8 of row
+// 8i + l%8 (i = 0, 1).  A DPP row rotation by 8 with bank masks then moves
+// the chunks so that lane (n = l%16, g = l/16) holds chunks 2g and 2g+1 of
+// row n, which is the B-fragment layout (columns of lane group g: a
+// contiguous quarter of the stage).  Half-line or quarter-line accesses,
+// which the fragment layout would give if loaded directly, stream
+// measurably slower from HBM.
+//
+// A ring of D stages per wave keeps loads in flight while the matrix cores
+// work; activations are loaded with their stage (the wait counter is in
+// order, so a late activation load would drain the ring).
+#include "moe_internal.h"
+
+namespace moe {
+
+namespace {
+
+constexpr int kWaves = 2;  // waves per block; they split the reduction of 16 rows
+
+template <class T>
+__device__ inline const __attribute__((address_space(1))) T* gmem(const T* p) {
+  return (const __attribute__((address_space(1))) T*)p;
+}
+__device__ inline f16x2 as_h2(uint32_t v) { return __builtin_bit_cast(f16x2, v); }
+__device__ inline uint32_t as_u32(f16x2 v) { return __builtin_bit_cast(uint32_t, v); }
+__device__ inline f16x8 pack8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  return __builtin_bit_cast(f16x8, u32x4{a, b, c, d});
+}
+
+// Geometry of one stage.
+template <int BITS> struct Geo {
+  static constexpr int kCols = 1024 / BITS;      // 128 bytes of each row
+  static constexpr int kLaneCols = kCols / 4;    // columns of one lane group
+  static constexpr int kChunkCols = kCols / 8;   // columns of one 16-byte chunk
+  static constexpr int kSteps = kCols / 32;      // MFMA k-steps
+  static constexpr int kScales = BITS == 16 ? 0 : kLaneCols / kGroup;  // per lane
+  static constexpr int kDepth = BITS == 16 ? 4 : (BITS == 4 ? 2 : 1);
+};
+
+// DPP: lane i of each 16-lane row reads lane i^8 (rotation by 8); BANKS
+// picks the 4-lane banks that take the moved value, the rest keep `old`.
+constexpr int kRowRor8 = 0x128;
+template <int BANKS>
+__device__ inline uint32_t dpp8(uint32_t old, uint32_t src) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)src, kRowRor8, 0xF, BANKS, false);
+}
+
+// One stage of one matrix: the two raw 16-byte loads and, for codes, the
+// scales of this lane's two chunks (packed f16 pairs).
+template <int BITS> struct WStage {
+  u32x4 v[2];
+  uint32_t s[BITS == 2 ? 2 : 1];
+};
+
+// Per-lane sources of one matrix for one 16-row tile.
+template <int BITS> struct WSrc {
+  const uint8_t* row;    // load lane's row and chunk (the second load adds row8)
+  int64_t row8;          // bytes between the two loads (8 rows)
+  const f16* srow;       // scales of row n, from this lane group's first group
+  int chunk;             // chunk index of the load lane (l / 8)
+  int ngr;               // groups per row
+};
+
+template <int BITS>
+__device__ inline WSrc<BITS> wsrc(const ExpertEntry& ex, int m, int64_t row0, int64_t ld) {
+  const int l = threadIdx.x & 63;
+  const int64_t rb = ld * BITS / 8;
+  const uint8_t* base = BITS == 16 ? reinterpret_cast<const uint8_t*>(ex.w[m]) : ex.q[m];
+  WSrc<BITS> s;
+  s.chunk = l >> 3;
+  s.row = base + (row0 + (l & 7)) * rb + 16 * s.chunk;
+  s.row8 = 8 * rb;
+  s.ngr = (int)(ld / kGroup);
+  s.srow = BITS == 16 ? nullptr
+                      : ex.s[m] + (row0 + (l & 15)) * s.ngr + Geo<BITS>::kScales * (l >> 4);
+  return s;
+}
+
+// Load stage kk (first column, a multiple of the stage width).  Chunks past
+// the row end (the last stage of a code row may be partial) read the row's
+// first chunk instead and get scale 0 at use; scales are read in group
+// pairs clamped to the row.  Nothing outside the row is touched.
+template <int BITS>
+__device__ inline void load_w(const WSrc<BITS>& s, int64_t kk, int64_t ld, WStage<BITS>& w) {
+  using G = const __attribute__((address_space(1))) u32x4*;
+  int64_t off = kk * BITS / 8;
+  if (BITS != 16) {
+    const bool ok = kk + (int64_t)(s.chunk + 1) * Geo<BITS>::kChunkCols <= ld;
+    off = ok ? off : -16 * (int64_t)s.chunk;
+  }
+  const uint8_t* p = s.row + off;
+  w.v[0] = __builtin_nontemporal_load(reinterpret_cast<G>(gmem(p)));
+  w.v[1] = __builtin_nontemporal_load(reinterpret_cast<G>(gmem(p + s.row8)));
+  if (BITS != 16) {
+    using S = const __attribute__((address_space(1))) uint32_t*;
+    const int g = (threadIdx.x & 63) >> 4;
+    const int gi = (int)(kk / kGroup) + Geo<BITS>::kScales * g;  // first group of the lane
+#pragma unroll
+    for (int h = 0; h < (BITS == 2 ? 2 : 1); ++h) {
+      const int idx = min(gi + 2 * h, s.ngr - 2);
+      w.s[h] = __builtin_nontemporal_load(
+          reinterpret_cast<S>(gmem(s.srow - Geo<BITS>::kScales * g + idx)));
+    }
+  }
+}
+
+// B fragments of this lane after the exchange: chunk 2g (c0) and 2g+1 (c1)
+// of row n, 4 dwords each.
+template <int BITS>
+__device__ inline void exchange(const WStage<BITS>& w, u32x4& c0, u32x4& c1) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    c0[d] = dpp8<0xC>(w.v[0][d], w.v[1][d]);  // lanes l%16 >= 8 take v1 of lane l^8
+    c1[d] = dpp8<0x3>(w.v[1][d], w.v[0][d]);  // lanes l%16 < 8 take v0 of lane l^8
+  }
+}
+
+// 8 int4 codes (one dword, element e at bits 4e) -> f16x8 times scale.
+// Each 16-bit half h becomes h | h << 12 so the nibble pairs sit at bits
+// (0, 16) and (8, 24); 0x6400 | u is 1024 + u.
+__device__ inline f16x8 deq4(uint32_t w, f16x2 s2) {
+  const uint32_t lo = w & 0xFFFFu, hi = w >> 16;
+  const uint32_t z0 = lo | (lo << 12), z1 = hi | (hi << 12);
+  const f16x2 bias = as_h2(0x64086408u);  // 1024 + 8
+  return pack8(as_u32((as_h2((z0 & 0x000F000Fu) | 0x64006400u) - bias) * s2),
+               as_u32((as_h2(((z0 >> 8) & 0x000F000Fu) | 0x64006400u) - bias) * s2),
+               as_u32((as_h2((z1 & 0x000F000Fu) | 0x64006400u) - bias) * s2),
+               as_u32((as_h2(((z1 >> 8) & 0x000F000Fu) | 0x64006400u) - bias) * s2));
+}
+
+// 8 int2 codes (16 bits, element e at bits 2e) -> f16x8 times scale;
+// z = h | h << 14 puts e_{2k} at bit 4k and e_{2k+1} at 4k + 16.
+__device__ inline f16x8 deq2(uint32_t h, f16x2 s2) {
+  const uint32_t z = h | (h << 14);
+  const f16x2 bias = as_h2(0x64026402u);  // 1024 + 2
+  return pack8(as_u32((as_h2((z & 0x00030003u) | 0x64006400u) - bias) * s2),
+               as_u32((as_h2(((z >> 4) & 0x00030003u) | 0x64006400u) - bias) * s2),
+               as_u32((as_h2(((z >> 8) & 0x00030003u) | 0x64006400u) - bias) * s2),
+               as_u32((as_h2(((z >> 12) & 0x00030003u) | 0x64006400u) - bias) * s2));
+}
+
+// Activation fragments of one stage: lane (t, g) holds columns
+// kk + kLaneCols g + 8j .. +7 of its token row for the steps j.  Chunks past
+// the row end read column 0 instead (their weights are zero).
+template <int BITS> struct AStage {
+  f16x8 a[Geo<BITS>::kSteps];
+};
+
+template <int BITS>
+__device__ inline void load_a(const f16* arow, int64_t kk, int64_t ld, AStage<BITS>& a) {
+  using GG = Geo<BITS>;
+  const int g = (threadIdx.x & 63) >> 4;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    int64_t col = kk + GG::kLaneCols * g + GG::kChunkCols * c;
+    if (BITS != 16) col = col + GG::kChunkCols <= ld ? col : 0;
+#pragma unroll
+    for (int j = 0; j < GG::kSteps / 2; ++j)
+      a.a[c * (GG::kSteps / 2) + j] = *reinterpret_cast<const f16x8*>(arow + col + 8 * j);
+  }
+}
+
+// Scales of this lane's chunks for stage kk, zero for chunks past the end:
+// sc[c][q] multiplies the q-th quantisation group of chunk c.
+template <int BITS>
+__device__ inline void chunk_scales(const WStage<BITS>& w, int64_t kk, int64_t ld,
+                                    f16x2 (&sc)[2][2]) {
+  using GG = Geo<BITS>;
+  const int g = (threadIdx.x & 63) >> 4;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const bool ok = kk + GG::kLaneCols * g + GG::kChunkCols * (c + 1) <= ld;
+    if (BITS == 4) {  // one group per chunk: halves of s[0]
+      const f16 v = as_h2(w.s[0])[c];
+      sc[c][0] = sc[c][1] = ok ? f16x2{v, v} : f16x2{0, 0};
+    } else {          // two groups per chunk: s[c]
+      const f16x2 p = as_h2(w.s[c]);
+      sc[c][0] = ok ? f16x2{p[0], p[0]} : f16x2{0, 0};
+      sc[c][1] = ok ? f16x2{p[1], p[1]} : f16x2{0, 0};
+    }
+  }
+}
+
+// acc[m] += A . W_m over one stage.
+template <int BITS, int NM>
+__device__ inline void consume(const WStage<BITS> (&w)[NM], const AStage<BITS>& a, int64_t kk,
+                               int64_t ld, f32x4 (&acc)[NM]) {
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    u32x4 c0, c1;
+    exchange<BITS>(w[m], c0, c1);
+    if (BITS == 16) {
+      acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[0], __builtin_bit_cast(f16x8, c0), acc[m], 0, 0, 0);
+      acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[1], __builtin_bit_cast(f16x8, c1), acc[m], 0, 0, 0);
+    } else {
+      f16x2 sc[2][2];
+      chunk_scales<BITS>(w[m], kk, ld, sc);
+      constexpr int kHalf = Geo<BITS>::kSteps / 2;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+#pragma unroll
+        for (int j = 0; j < kHalf; ++j) {
+          const uint32_t word = c == 0 ? c0[BITS == 4 ? j : j / 2] : c1[BITS == 4 ? j : j / 2];
+          f16x8 b;
+          if (BITS == 4) b = deq4(word, sc[c][0]);
+          else b = deq2((word >> (16 * (j & 1))) & 0xFFFFu, sc[c][j / 4]);
+          acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[c * kHalf + j], b, acc[m], 0, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+// acc[m] (C tile: 16 tokens x 16 rows) = A(tokens, S) . W_m(rows, S)^T for
+// the 16-row tile at row0 of the matrices mats[], over this wave's stages
+// S = {wave, wave + kWaves, ...}: the waves of a block interleave 128-byte
+// stages of the same rows.  Every load is unconditional (ring slots past
+// the wave's last stage reload it and are not multiplied) so that the
+// compiler's wait counts stay exact and the steady-state loop carries no
+// branch.
+template <int BITS, int NM>
+__device__ inline void tile_gemm(const ExpertEntry& ex, const int (&mats)[NM], int64_t row0,
+                                 int64_t ld, const f16* arow, int wave, f32x4 (&acc)[NM]) {
+  using GG = Geo<BITS>;
+  constexpr int D = GG::kDepth;
+  const int64_t nst = ((ld + GG::kCols - 1) / GG::kCols - wave + kWaves - 1) / kWaves;
+  if (nst <= 0) return;
+  WSrc<BITS> src[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) src[m] = wsrc<BITS>(ex, mats[m], row0, ld);
+  auto col = [&](int64_t i) { return (wave + (i < nst ? i : nst - 1) * kWaves) * (int64_t)GG::kCols; };
+  WStage<BITS> w[D][NM];
+  AStage<BITS> a[D];
+#pragma unroll
+  for (int u = 0; u < D; ++u) {
+    const int64_t kk = col(u);
+#pragma unroll
+    for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
+    load_a<BITS>(arow, kk, ld, a[u]);
+  }
+  int64_t i0 = 0;
+  for (; i0 + D <= nst; i0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      consume<BITS, NM>(w[u], a[u], col(i0 + u), ld, acc);
+      const int64_t kk = col(i0 + u + D);
+#pragma unroll
+      for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
+      load_a<BITS>(arow, kk, ld, a[u]);
+      // keep the ring order: the scheduler would otherwise sink the loads
+      // below the products and wait for nearly all of them each round
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  // the last nst - i0 < D stages sit in slots 0 .. nst - i0 - 1
+#pragma unroll
+  for (int u = 0; u < D - 1; ++u)
+    if (u < nst - i0) consume<BITS, NM>(w[u], a[u], col(i0 + u), ld, acc);
+}
+
+// Sum of the waves' partial tiles in a fixed order; the result is valid in
+// wave 0.  red holds kWaves * NM * 256 floats.
+template <int NM>
+__device__ inline void block_sum(f32x4 (&acc)[NM], float* red) {
+  const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+    *reinterpret_cast<f32x4*>(red + ((wave * NM + m) * 64 + l) * 4) = acc[m];
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int v = 1; v < kWaves; ++v)
+        acc[m] += *reinterpret_cast<const f32x4*>(red + ((v * NM + m) * 64 + l) * 4);
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- up-proj
+template <int BITS>
+__device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* perm,
+                         const f16* x, f16* h, int d, int f, int K, int64_t row0, float* red) {
+  const int l = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int mats[2] = {0, 1};
+  for (int j0 = 0; j0 < g.count; j0 += 16) {
+    const int n = min(16, g.count - j0);
+    const int32_t* pairs = perm + g.offset + j0;
+    // lanes past the last token repeat it: row m of the product depends on
+    // row m of A only, and those rows are not stored
+    const f16* arow = x + (int64_t)(pairs[min(l & 15, n - 1)] / K) * d;
+    f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+    tile_gemm<BITS, 2>(ex, mats, row0, d, arow, wave, acc);
+    block_sum<2>(acc, red);
+    if (wave == 0) {
+      const int64_t row = row0 + (l & 15);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = 4 * (l >> 4) + i;
+        if (tok < n) {
+          const float a = acc[0][i], b = acc[1][i];
+          h[(int64_t)pairs[tok] * f + row] = (f16)(a / (1.0f + expf(-a)) * b);
+        }
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(64 * kWaves, 2) void decode_up_mfma_kernel(
+    const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
+    const int32_t* __restrict__ perm, const f16* __restrict__ x, f16* __restrict__ h,
+    int d, int f, int K) {
+  __shared__ float red[kWaves * 2 * 256];
+  if ((int)blockIdx.y >= wl->n_groups) return;
+  const Group g = wl->groups[blockIdx.y];
+  const ExpertEntry ex = table[g.expert];
+  const int64_t row0 = (int64_t)blockIdx.x * 16;
+  if (g.bits == 16) up_group<16>(ex, g, perm, x, h, d, f, K, row0, red);
+  else if (g.bits == 4) up_group<4>(ex, g, perm, x, h, d, f, K, row0, red);
+  else up_group<2>(ex, g, perm, x, h, d, f, K, row0, red);
+}
+
+// -------------------------------------------------------------- down-proj
+template <int BITS>
+__device__ void down_group(const ExpertEntry& ex, const Group& g, const int32_t* perm,
+                           const f16* h, float* e, int d, int f, int64_t row0, float* red) {
+  const int l = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int mats[1] = {2};
+  for (int j0 = 0; j0 < g.count; j0 += 16) {
+    const int n = min(16, g.count - j0);
+    const int32_t* pairs = perm + g.offset + j0;
+    const f16* arow = h + (int64_t)pairs[min(l & 15, n - 1)] * f;
+    f32x4 acc[1] = {f32x4{0, 0, 0, 0}};
+    tile_gemm<BITS, 1>(ex, mats, row0, f, arow, wave, acc);
+    block_sum<1>(acc, red);
+    if (wave == 0) {
+      const int64_t row = row0 + (l & 15);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = 4 * (l >> 4) + i;
+        if (tok < n) e[(int64_t)(g.offset + j0 + tok) * d + row] = acc[0][i];
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(64 * kWaves, 2) void decode_down_mfma_kernel(
+    const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
+    const int32_t* __restrict__ perm, const f16* __restrict__ h, float* __restrict__ e,
+    int d, int f) {
+  __shared__ float red[kWaves * 256];
+  if ((int)blockIdx.y >= wl->n_groups) return;
+  const Group g = wl->groups[blockIdx.y];
+  const ExpertEntry ex = table[g.expert];
+  const int64_t row0 = (int64_t)blockIdx.x * 16;
+  if (g.bits == 16) down_group<16>(ex, g, perm, h, e, d, f, row0, red);
+  else if (g.bits == 4) down_group<4>(ex, g, perm, h, e, d, f, row0, red);
+  else down_group<2>(ex, g, perm, h, e, d, f, row0, red);
+}
+
+}  // namespace
+
+hipError_t launch_decode_up_mfma(const ExpertEntry* table, const WorkList* wl,
+                                 const int32_t* perm, const f16* x, f16* h, int d,
+                                 int f, int K, int max_groups, hipStream_t s) {
+  dim3 grid(f / 16, max_groups);
+  decode_up_mfma_kernel<<<grid, 64 * kWaves, 0, s>>>(table, wl, perm, x, h, d, f, K);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_down_mfma(const ExpertEntry* table, const WorkList* wl,
+                                   const int32_t* perm, const f16* h, float* e_perm,
+                                   int d, int f, int max_groups, hipStream_t s) {
+  dim3 grid(d / 16, max_groups);
+  decode_down_mfma_kernel<<<grid, 64 * kWaves, 0, s>>>(table, wl, perm, h, e_perm, d, f);
+  return hipGetLastError();
+}
+
+}  // namespace moe

@@ -64,7 +64,7 @@ struct moe_layer {
   float* d_w = nullptr;
   int8_t* d_prec = nullptr;
   f16* d_h = nullptr;       // [max_tokens*K, f]
-  float* d_eperm = nullptr; // prefill expert outputs in group order: [max_tokens*K, d]
+  float* d_eperm = nullptr; // per-pair expert outputs in group order: [max_tokens*K, d]
   void* arena = nullptr;
   // stage timing (measurement only): 5 events per recorded call
   bool timing = false;
@@ -163,6 +163,8 @@ hipError_t mark(moe_layer* l, int slot, hipStream_t s) {
   return hipEventRecord(l->ev_pool[at], s);
 }
 
+constexpr int kDecodeMfmaMinTokens = 3;
+
 moe_status decode_impl(moe_layer* l, int32_t T, const void* x, float* y,
                        float* h_res, void* x_next, int32_t* idx, float* w,
                        int8_t* prec, void* stream) {
@@ -179,15 +181,29 @@ moe_status decode_impl(moe_layer* l, int32_t T, const void* x, float* y,
   HIP_TRY(launch_route_decode(route_params(l, T, x), route_out(l, idx, w, prec),
                               l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
   HIP_TRY(mark(l, 1, s), "timing event");
-  HIP_TRY(launch_decode_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
-                           l->d_h, T, d, f, K, mg, s), "up kernel launch");
-  HIP_TRY(mark(l, 2, s), "timing event");
-  HIP_TRY(launch_decode_down(l->d_table, l->d_wl, l->d_perm, l->d_w, l->d_h, y, h_res,
-                             T, d, f, K, s), "down kernel launch");
-  HIP_TRY(mark(l, 3, s), "timing event");
-  if (h_res)
-    HIP_TRY(launch_rmsnorm(h_res, static_cast<f16*>(x_next), T, d, l->desc.rms_eps, s),
-            "rmsnorm kernel launch");
+  if (T >= kDecodeMfmaMinTokens) {
+    // several tokens per step: matrix-core kernels, per-pair down rows and
+    // the fused combine (+ residual rmsnorm) of the prefill path
+    HIP_TRY(launch_decode_up_mfma(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
+                                  l->d_h, d, f, K, mg, s), "up kernel launch");
+    HIP_TRY(mark(l, 2, s), "timing event");
+    HIP_TRY(launch_decode_down_mfma(l->d_table, l->d_wl, l->d_perm, l->d_h, l->d_eperm,
+                                    d, f, mg, s), "down kernel launch");
+    HIP_TRY(launch_combine_prefill(l->d_eperm, l->d_pos, l->d_w, l->d_prec, T, d, K, y, h_res,
+                                   static_cast<f16*>(x_next), l->desc.rms_eps, s),
+            "combine kernel launch");
+    HIP_TRY(mark(l, 3, s), "timing event");
+  } else {
+    HIP_TRY(launch_decode_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
+                             l->d_h, T, d, f, K, mg, s), "up kernel launch");
+    HIP_TRY(mark(l, 2, s), "timing event");
+    HIP_TRY(launch_decode_down(l->d_table, l->d_wl, l->d_perm, l->d_w, l->d_h, y, h_res,
+                               T, d, f, K, s), "down kernel launch");
+    HIP_TRY(mark(l, 3, s), "timing event");
+    if (h_res)
+      HIP_TRY(launch_rmsnorm(h_res, static_cast<f16*>(x_next), T, d, l->desc.rms_eps, s),
+              "rmsnorm kernel launch");
+  }
   HIP_TRY(mark(l, 4, s), "timing event");
   return MOE_OK;
 }

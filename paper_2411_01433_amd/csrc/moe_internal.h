@@ -88,6 +88,12 @@ hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
                               const int32_t* perm, const float* gate_w,
                               const f16* h, float* y, float* h_res, int T, int d,
                               int f, int K, hipStream_t s);
+hipError_t launch_decode_up_mfma(const ExpertEntry* table, const WorkList* wl,
+                                 const int32_t* perm, const f16* x, f16* h, int d,
+                                 int f, int K, int max_groups, hipStream_t s);
+hipError_t launch_decode_down_mfma(const ExpertEntry* table, const WorkList* wl,
+                                   const int32_t* perm, const f16* h, float* e_perm,
+                                   int d, int f, int max_groups, hipStream_t s);
 hipError_t launch_rmsnorm(const float* h_res, f16* x_next, int T, int d,
                           float eps, hipStream_t s);
 hipError_t launch_prefill_up(const ExpertEntry* table, const WorkList* wl,

@@ -223,6 +223,18 @@ def test_many_tokens_per_expert():
                 t1=0.4, t2=1.0)
 
 
+@pytest.mark.parametrize("T", [1, 2, 3, 4, 9, 16, 17])
+def test_token_counts_both_decode_kernels(T):
+    """Steps of one or two tokens take the dot2 kernels, larger steps the
+    matrix-core kernels; every tag kind, ragged d and f, groups of more than
+    16 tokens at T = 17 (K = E)."""
+    wl = _edge("edge_tokens", 36, 320, 448, 5, 5, T,
+               [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4, C.TAG_MISS_INT2],
+               t1=0.3, t2=0.8)
+    rng = np.random.default_rng(100 + T)
+    _layer_case(wl, wl.fixed_tags, rng.standard_normal((T, 320)).astype(np.float16))
+
+
 def test_top1():
     wl = _edge("edge_top1", 35, 256, 256, 8, 1, 7, [C.TAG_INT4] * 8)
     rng = np.random.default_rng(6)
