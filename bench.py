@@ -19,12 +19,23 @@ Prints one JSON line on stdout (progress goes to stderr):
                  launch stream, against the 8 TB/s HBM peak
   cpu_baseline   the float64 CPU oracle timed on the host cores on a
                  bounded sample of the same workload
+
+Counter modes (run under rocprofv3 --pmc; they print one JSON line):
+  --copy-calibration   a plain 256 MiB device copy, 5 launches, to scale the
+                       FETCH_SIZE / WRITE_SIZE counters to bytes
+  --pmc-pass           only the warmup + timed decode steps, with the mean
+                       algorithmic up-projection bytes of those launches
+The roofline "traffic" field is read from the committed counter summary
+profiles/decode_up_mixtral_t1_pmc.md and is null when the decode kernel
+source has changed since those counters were taken.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -37,6 +48,35 @@ sys.path.insert(0, os.path.join(ROOT, "tests"))
 METRIC = ("MoE-layer decode tokens/s + effective weight GB/s (% of HBM peak), 1 GPU")
 HBM_PEAK_GBPS = 8000.0
 N_STREAMS = 64
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "decode_up_mixtral_t1_pmc.md")
+UP_KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_01433_amd", "csrc", "decode.hip")
+
+
+def source_sha256(path=UP_KERNEL_SOURCE):
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch of the up-projection kernel from the committed
+    counter summary: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
+    scaled by what the counter reads for a copy of known size.  None when
+    there is no summary for this workload or the kernel source changed."""
+    try:
+        text = open(PMC_SUMMARY).read()
+    except OSError:
+        return None, "no counter summary"
+    m = re.search(r"<!-- traffic-json (\{.*?\}) -->", text, re.S)
+    if not m:
+        return None, "no traffic record in the counter summary"
+    rec = json.loads(m.group(1))
+    if rec.get("workload") != workload:
+        return None, "counter summary is for another workload"
+    if rec.get("source_sha256") != source_sha256():
+        return None, "decode kernel source changed since the counters were taken"
+    b = (rec["fetch_kib_per_dispatch"] * rec["fetch_factor"]
+         + rec["write_kib_per_dispatch"] * rec["write_factor"]) * 1024.0
+    return b, "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
 
 
 def log(*a):
@@ -138,6 +178,11 @@ def run_decode_layer(args):
     ms = ev0.elapsed_time(ev1) / args.steps
 
     idx_h, prec_h = idx.cpu().numpy(), prec.cpu().numpy()
+    if args.pmc_pass:
+        ups = [step_bytes(wl, idx_h[i], prec_h[i], tags)[1] for i in range(n_all)]
+        return {"mode": "pmc-pass", "workload": wl.name, "launches": n_all,
+                "up_bytes_per_launch_mean": float(np.mean(ups)),
+                "source_sha256": source_sha256()}, None
     per = [step_bytes(wl, idx_h[i], prec_h[i], tags) for i in range(args.warmup, n_all)]
     b_total = float(np.mean([p[0] for p in per]))
     b_up = float(np.mean([p[1] for p in per]))
@@ -153,6 +198,16 @@ def run_decode_layer(args):
     ev1.record()
     torch.cuda.synchronize()
     ms_hot = ev0.elapsed_time(ev1) / hot_steps
+
+    # per-step distribution: one event between consecutive steps
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record()
+    for j, i in enumerate(range(args.warmup, n_all)):
+        step(i)
+        evs[j + 1].record()
+    torch.cuda.synchronize()
+    per_step = np.array([evs[j].elapsed_time(evs[j + 1]) * 1e3 for j in range(args.steps)])
+    q10, q50, q90 = (float(v) for v in np.percentile(per_step, [10, 50, 90]))
 
     # stage-timed pass (events between kernels on the launch stream)
     log("stage timing pass")
@@ -175,6 +230,7 @@ def run_decode_layer(args):
     event_us = stage_us[3]
     up_us = stage_us[1] - event_us
     achieved = b_up / (up_us * 1e-6) / 1e9
+    traffic, traffic_note = measured_traffic(wl.name)
 
     out = {
         "metric": METRIC,
@@ -192,11 +248,13 @@ def run_decode_layer(args):
         "pct_hbm_peak": 100.0 * b_total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": b_total,
         "hot_tokens_per_s": T / (ms_hot * 1e-3),
+        "step_us_p10_p50_p90": [q10, q50, q90],
         "stage_us": dict(zip(["route", "up", "down_combine", "empty"], stage_us)),
         "event_overhead_us": event_us,
         "roofline": {"bound": "hbm", "kernel": "decode_up_kernel",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "traffic_source": traffic_note,
                      "bytes_per_launch": b_up, "mean_launch_us": up_us,
                      "timing": "HIP events between kernels on the launch stream, "
                                "minus the same run's empty-stage event overhead"},
@@ -372,6 +430,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--cpu-tokens", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="warmup + timed decode steps only (for counter runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="plain 256 MiB device copy x5 (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this library runs the layer on a "
@@ -382,6 +444,17 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        n = 256 << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "copy-calibration", "bytes_read_per_launch": n,
+                          "bytes_written_per_launch": n, "launches": 5}), flush=True)
+        return
     import paper_2411_01433_amd as P
     P.lib()
     from synth import configs as C
@@ -390,7 +463,7 @@ def main():
         print(json.dumps(out), flush=True)
         return
     out, state = run_decode_layer(args)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.pmc_pass:
         parity_and_cpu(args, state, out)
     print(json.dumps(out), flush=True)
 
