@@ -17,6 +17,7 @@ namespace moe {
 namespace {
 
 constexpr int kRouteThreads = 1024;
+static_assert(kMaxExperts <= kRouteThreads, "one thread per expert stages the table");
 constexpr int kPrefillTokPerBlock = 1;
 constexpr int kPrefillThreads = 256;
 
@@ -34,47 +35,62 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
-// Dot products of tokens [t0, t1) against all E gate rows; one wave per
-// (token, expert) pair, 8 fp16 per lane per 512-column chunk.  A batch of 8
-// chunks is loaded before any arithmetic so the loads overlap.  Results go
+// Dot products of tokens [t0, t1) against all E gate rows.  One wave per
+// (expert, batch of up to TB tokens): the gate row chunk is loaded once and
+// used for every token of the batch; KB chunks of 512 columns (8 fp16 per
+// lane) of the gate row and of each token are loaded before any arithmetic
+// so that the loads overlap (one memory latency per KB chunks).  Results go
 // to lg[t-t0][e].
+template <int TB, int KB>
 __device__ void gate_logits(const RouteParams& p, int t0, int t1, float* lg) {
-  constexpr int kBatch = 8;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int n_waves = blockDim.x >> 6;
-  const int n_pairs = (t1 - t0) * p.E;
-  for (int q = wave; q < n_pairs; q += n_waves) {
-    const int tl = q / p.E;
-    const int e = q - tl * p.E;
-    const f16* xr = p.x + (int64_t)(t0 + tl) * p.d;
+  const int n_tb = (t1 - t0 + TB - 1) / TB;
+  const int n_items = n_tb * p.E;
+  for (int q = wave; q < n_items; q += n_waves) {
+    const int e = q % p.E;
+    const int tb0 = t0 + (q / p.E) * TB;
+    const int nt = min(TB, t1 - tb0);
     const f16* gr = p.wg + (int64_t)e * p.d;
-    float acc = 0.0f;
-    for (int c0 = 0; c0 < p.d; c0 += kBatch * 512) {
-      u32x4 a[kBatch], b[kBatch];
+    float acc[TB];
 #pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
+    for (int i = 0; i < TB; ++i) acc[i] = 0.0f;
+    for (int c0 = 0; c0 < p.d; c0 += KB * 512) {
+      u32x4 b[KB], a[TB][KB];
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
         const int c = c0 + j * 512 + lane * 8;
-        a[j] = c < p.d ? *reinterpret_cast<const u32x4*>(xr + c) : u32x4{0, 0, 0, 0};
         b[j] = c < p.d ? *reinterpret_cast<const u32x4*>(gr + c) : u32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int i = 0; i < TB; ++i)
+          a[i][j] = (i < nt && c < p.d)
+                        ? *reinterpret_cast<const u32x4*>(p.x + (int64_t)(tb0 + i) * p.d + c)
+                        : u32x4{0, 0, 0, 0};
       }
 #pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        acc = dot2(a[j].x, b[j].x, acc);
-        acc = dot2(a[j].y, b[j].y, acc);
-        acc = dot2(a[j].z, b[j].z, acc);
-        acc = dot2(a[j].w, b[j].w, acc);
-      }
+      for (int i = 0; i < TB; ++i)
+#pragma unroll
+        for (int j = 0; j < KB; ++j) {
+          acc[i] = dot2(a[i][j].x, b[j].x, acc[i]);
+          acc[i] = dot2(a[i][j].y, b[j].y, acc[i]);
+          acc[i] = dot2(a[i][j].z, b[j].z, acc[i]);
+          acc[i] = dot2(a[i][j].w, b[j].w, acc[i]);
+        }
     }
-    acc = wave_sum(acc);
-    if (lane == 0) lg[tl * p.E + e] = acc;
+#pragma unroll
+    for (int i = 0; i < TB; ++i) {
+      const float v = wave_sum(acc[i]);
+      if (lane == 0 && i < nt) lg[(tb0 - t0 + i) * p.E + e] = v;
+    }
   }
 }
 
 // top-k, softmax over the selected logits and the Eq. 2 rule for one token;
 // tags[e] is the expert table's tag column staged in LDS.
 __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
-                             const int* tags, RouteOut o) {
+                             const int* tags, RouteOut o, int32_t* s_idx = nullptr,
+                             int8_t* s_prec = nullptr) {
   int sel[kMaxTopK];
   float ls[kMaxTopK];
   uint64_t taken = 0;  // E <= 64
@@ -119,6 +135,10 @@ __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
     o.idx[pi] = e;
     o.w[pi] = w;
     o.prec[pi] = (int8_t)prec;
+    if (s_idx) {
+      s_idx[pi] = e;
+      s_prec[pi] = (int8_t)prec;
+    }
     if (o.user_idx) o.user_idx[pi] = e;
     if (o.user_w) o.user_w[pi] = w;
     if (o.user_prec) o.user_prec[pi] = (int8_t)prec;
@@ -208,8 +228,7 @@ __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
   }
 }
 
-// Expert tags and low-copy widths into LDS (issued before the gate loads so
-// the two memory round trips overlap).
+// Expert tags and low-copy widths into LDS.
 __device__ inline void stage_table(const RouteParams& p, int* tags, int* low_bits) {
   for (int e = threadIdx.x; e < p.E; e += blockDim.x) {
     tags[e] = p.table[e].tag;
@@ -217,18 +236,42 @@ __device__ inline void stage_table(const RouteParams& p, int* tags, int* low_bit
   }
 }
 
+// The same in two halves: the loads are issued before the gate loads and
+// the LDS stores after them, so the two memory round trips overlap (E is at
+// most 64, below the block size).
+struct TableRow {
+  int tag, low_bits;
+  __device__ inline void load(const RouteParams& p) {
+    const int e = threadIdx.x;
+    tag = e < p.E ? p.table[e].tag : 0;
+    low_bits = e < p.E ? p.table[e].low_bits : 0;
+  }
+  __device__ inline void store(const RouteParams& p, int* tags, int* lb) const {
+    if ((int)threadIdx.x < p.E) {
+      tags[threadIdx.x] = tag;
+      lb[threadIdx.x] = low_bits;
+    }
+  }
+};
+
 // Decode: one block routes every token and builds the work list.
 __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
     RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
   __shared__ float lg[kDecodeMaxTokens * kMaxExperts];
   __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
-  stage_table(p, tags, low_bits);
-  gate_logits(p, 0, p.T, lg);
+  __shared__ int32_t s_idx[kDecodeMaxTokens * kMaxTopK];
+  __shared__ int8_t s_prec[kDecodeMaxTokens * kMaxTopK];
+  TableRow tr;
+  tr.load(p);
+  if (p.T == 1) gate_logits<1, 8>(p, 0, p.T, lg);
+  else if (p.T == 2) gate_logits<2, 8>(p, 0, p.T, lg);
+  else gate_logits<4, 4>(p, 0, p.T, lg);
+  tr.store(p, tags, low_bits);
   __syncthreads();
   for (int t = threadIdx.x; t < p.T; t += blockDim.x)
-    decide_token(p, t, lg + t * p.E, tags, o);
+    decide_token(p, t, lg + t * p.E, tags, o, s_idx, s_prec);
   __syncthreads();
-  build_worklist(p, o.idx, o.prec, low_bits, wl, perm, pos);
+  build_worklist(p, s_idx, s_prec, low_bits, wl, perm, pos);
 }
 
 // Prefill: many blocks route their tokens; a second kernel builds the list.
@@ -239,7 +282,7 @@ __global__ __launch_bounds__(kPrefillThreads) void route_tokens_kernel(
   const int t0 = blockIdx.x * kPrefillTokPerBlock;
   const int t1 = min(t0 + kPrefillTokPerBlock, p.T);
   stage_table(p, tags, low_bits);
-  gate_logits(p, t0, t1, lg);
+  gate_logits<kPrefillTokPerBlock, 8>(p, t0, t1, lg);
   __syncthreads();
   for (int t = t0 + (int)threadIdx.x; t < t1; t += blockDim.x)
     decide_token(p, t, lg + (t - t0) * p.E, tags, o);
