@@ -251,7 +251,9 @@ def run_decode_layer(args):
         "step_us_p10_p50_p90": [q10, q50, q90],
         "stage_us": dict(zip(["route", "up", "down_combine", "empty"], stage_us)),
         "event_overhead_us": event_us,
-        "roofline": {"bound": "hbm", "kernel": "decode_up_kernel",
+        "roofline": {"bound": "hbm",
+                     # the library takes the matrix-core kernels from 3 tokens per step
+                     "kernel": "decode_up_kernel" if T < 3 else "decode_up_mfma_kernel",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
                      "traffic_source": traffic_note,
