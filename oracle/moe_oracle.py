@@ -334,6 +334,58 @@ def residual_step(h: np.ndarray, y: np.ndarray, eps: float = RMS_EPS):
 
 
 # --------------------------------------------------------------------------
+# Adaptive Expert Predictor: the Stacking Computer (Section 3.3, "Expert
+# predictor design", Fig. 7).
+# --------------------------------------------------------------------------
+@dataclass
+class Prediction:
+    idx: np.ndarray      # [T, p, K] predicted experts of layers l+1 .. l+p
+    w: np.ndarray        # [T, p, K] their normalised gate values
+    logits: np.ndarray   # [T, p, E]
+    first_miss: int      # first j in 1..p with a predicted expert not cached; 0 if none
+    preload: int         # bitmask of the predicted experts of layer first_miss not cached
+
+
+def predict_next_layers(x16: np.ndarray, wg16_next, cached, k: int,
+                        forced_idx: np.ndarray | None = None) -> Prediction:
+    """Predicted experts of the next p layers from the current layer's gating
+    input (Section 3.3): gating inputs of consecutive layers are similar, so
+    the gate of layer l+j applied to layer l's input predicts layer l+j's
+    choice; each prediction uses that layer's own top-k and normalisation.
+    Walking j = 1, 2, ..., p, prediction continues while every predicted
+    expert of layer l+j is in the expert cache and stops at the first layer
+    with a missing one, whose missing experts are the ones to preload.
+    ``cached[j-1]`` is the bitmask of layer l+j's cached experts.  The
+    Stacking Computer evaluates the p gates as one stacked product; here
+    they are p independent routers.  ``forced_idx`` [T, p, K] replaces the
+    top-k choice where the comparison flagged a near-tie."""
+    x = np.asarray(x16)
+    p = len(wg16_next)
+    T = x.shape[0]
+    E = np.asarray(wg16_next[0]).shape[0]
+    idx = np.zeros((T, p, k), dtype=np.int64)
+    w = np.zeros((T, p, k), dtype=np.float64)
+    logits = np.zeros((T, p, E), dtype=np.float64)
+    for j in range(p):
+        l = router_logits(x, wg16_next[j])
+        logits[:, j] = l
+        for t in range(T):
+            sel = topk(l[t], k) if forced_idx is None else np.asarray(forced_idx[t, j])
+            idx[t, j] = sel
+            w[t, j] = gate_weights(l[t, sel])
+    first, pre = 0, 0
+    for j in range(p):
+        need = 0
+        for e in idx[:, j].ravel():
+            need |= 1 << int(e)
+        miss = need & ~int(cached[j])
+        if miss:
+            first, pre = j + 1, miss
+            break
+    return Prediction(idx, w, logits, first, pre)
+
+
+# --------------------------------------------------------------------------
 # Brute-force variants (pure Python loops) used to pin the above.
 # --------------------------------------------------------------------------
 def brute_router_logits(x16, wg16):

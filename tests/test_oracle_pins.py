@@ -374,3 +374,63 @@ def test_rmsnorm_closed_form(rng):
     h2, x2 = O.residual_step(h, np.ones_like(h))
     np.testing.assert_allclose(h2, h + 1.0)
     assert x2.dtype == np.float16
+
+
+# ------------------------------------------ Stacking Computer (Section 3.3)
+def test_predictor_worked_example():
+    d = json.load(open(os.path.join(GOLDEN, "predictor_worked_example.json")))
+    x = np.array(d["x"], dtype=np.float16)
+    gates = [np.array(g, dtype=np.float16) for g in d["gates"]]
+    pr = O.predict_next_layers(x, gates, d["cached"], d["k"])
+    np.testing.assert_array_equal(pr.logits, np.array(d["logits"]))
+    assert pr.idx.tolist() == d["idx"]
+    np.testing.assert_allclose(pr.w, np.array(d["w"]), rtol=0, atol=1e-15)
+    assert (pr.first_miss, pr.preload) == (d["first_miss"], d["preload"])
+
+
+def test_predictor_one_layer_is_that_layers_router(rng):
+    x = _fp16(rng, (5, 48), 1.0)
+    wg = _fp16(rng, (8, 48), 0.3)
+    pr = O.predict_next_layers(x, [wg], [0], 2)
+    r = O.route(x, wg, [O.TAG_FP16] * 8, 2, 1.0, 1.0)
+    np.testing.assert_array_equal(pr.idx[:, 0], r.idx)
+    np.testing.assert_allclose(pr.w[:, 0], r.w, rtol=0, atol=0)
+
+
+def test_predictor_walk_brute_force(rng):
+    """Sets and the walk written out with Python sets on exhaustive top-k."""
+    T, d, E, K, p = 3, 16, 6, 2, 4
+    for trial in range(40):
+        x = _fp16(rng, (T, d), 1.0)
+        gates = [_fp16(rng, (E, d), 0.5) for _ in range(p)]
+        cached = [int(v) for v in rng.integers(0, 1 << E, size=p)]
+        if trial % 4 == 0:
+            cached = [(1 << E) - 1] * p
+        pr = O.predict_next_layers(x, gates, cached, K)
+        exp_first, exp_pre = 0, 0
+        for j in range(p):
+            need = set()
+            for t in range(T):
+                row = [sum(float(x[t, c]) * float(gates[j][e, c]) for c in range(d))
+                       for e in range(E)]
+                sel = O.brute_topk_set(row, K)
+                assert set(pr.idx[t, j].tolist()) == sel
+                need |= sel
+            missing = {e for e in need if not (cached[j] >> e) & 1}
+            if missing:
+                exp_first, exp_pre = j + 1, sum(1 << e for e in missing)
+                break
+        assert (pr.first_miss, pr.preload) == (exp_first, exp_pre)
+
+
+def test_predictor_walk_extremes(rng):
+    x = _fp16(rng, (4, 32), 1.0)
+    gates = [_fp16(rng, (8, 32), 0.5) for _ in range(3)]
+    full = O.predict_next_layers(x, gates, [0xFF] * 3, 2)
+    assert (full.first_miss, full.preload) == (0, 0)
+    none = O.predict_next_layers(x, gates, [0] * 3, 2)
+    union = 0
+    for e in none.idx[:, 0].ravel():
+        union |= 1 << int(e)
+    assert (none.first_miss, none.preload) == (1, union)
+    assert np.allclose(none.w.sum(axis=-1), 1.0)
