@@ -364,6 +364,58 @@ def run_stack(args):
     return out
 
 
+def run_predictor(args):
+    """Stacking Computer timing (Section 3.3, the comparison of Fig. 17a):
+    one stacked launch over the gates of p = 1..8 layers ahead against the
+    sequential way, p one-layer predictions launched one after the other.
+    One decode token; Mixtral-shaped (8 experts) and Phi-MoE-shaped (16)
+    gates.  The gates are small (64-128 KiB per layer) and stay in L2."""
+    import torch
+    import paper_2411_01433_amd as P
+    from synth import configs as C
+
+    res = {}
+    for wl in (C.MIXTRAL_PREFILL, C.PHI_STACK):
+        d, E, K, T = wl.d_model, wl.n_experts, wl.top_k, 1
+        gates = [torch.from_numpy(C.router_weight(wl, l)).cuda() for l in range(1, 9)]
+        x = torch.from_numpy(C.hidden_states(wl)[:T]).cuda()
+        stacked = {p: P.MoePredictor(d, E, K, T, gates[:p]) for p in range(1, 9)}
+        single = [P.MoePredictor(d, E, K, T, [g]) for g in gates]
+        cd = torch.zeros((8,), dtype=torch.int64, device="cuda")
+        fm = torch.empty((1,), dtype=torch.int32, device="cuda")
+        pre = torch.empty((1,), dtype=torch.int64, device="cuda")
+
+        def timed(fn, n):
+            for _ in range(10):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(n):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / n * 1e3
+
+        row = {}
+        for p in range(1, 9):
+            ip = torch.empty((T, p, K), dtype=torch.int32, device="cuda")
+            i1 = torch.empty((T, 1, K), dtype=torch.int32, device="cuda")
+            t_st = timed(lambda: stacked[p].predict(x, cd[:p], ip, fm, pre), args.steps)
+            t_seq = timed(lambda: [single[j].predict(x, cd[:1], i1, fm, pre)
+                                   for j in range(p)], args.steps)
+            row[p] = {"stacked_us": t_st, "sequential_us": t_seq}
+            log(f"{wl.name} p={p}: stacked {t_st:.2f} us, sequential {t_seq:.2f} us")
+        res[f"E{E}_d{d}"] = row
+        for pr in list(stacked.values()) + single:
+            pr.destroy()
+    return {"metric": "Stacking Computer: time per prediction vs layers ahead p",
+            "unit": "us", "tokens": 1, "steps": args.steps, "data": "synthetic",
+            "note": "stacked = one launch over the p stacked gates; sequential = p "
+                    "one-layer launches back to back on the stream",
+            "results": res}
+
+
 def parity_and_cpu(args, state, out):
     """Check sampled steps against the oracle and time the oracle itself."""
     import torch
@@ -436,6 +488,8 @@ def main():
                     help="warmup + timed decode steps only (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="plain 256 MiB device copy x5 (counter calibration)")
+    ap.add_argument("--predictor", action="store_true",
+                    help="time the Stacking Computer against sequential gates, p = 1..8")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this library runs the layer on a "
@@ -460,6 +514,9 @@ def main():
     import paper_2411_01433_amd as P
     P.lib()
     from synth import configs as C
+    if args.predictor:
+        print(json.dumps(run_predictor(args)), flush=True)
+        return
     if C.BY_NAME[args.workload].n_layers > 1:
         out = run_stack(args)
         print(json.dumps(out), flush=True)

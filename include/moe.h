@@ -187,6 +187,50 @@ moe_status moe_layer_stage_times(moe_layer_t layer, double* ms,
  * the device first).  The borrowed fp16 weights are not touched. */
 moe_status moe_layer_destroy(moe_layer_t layer);
 
+/* ---- Stacking Computer of the Adaptive Expert Predictor ----------------
+ * Section 3.3 ("Expert predictor design") and Fig. 7: gating inputs of
+ * consecutive layers are similar, so the gates of the next p layers
+ * applied to the current layer's gating input predict the experts those
+ * layers will select.  The p gates are stacked into one [p*E, d_model]
+ * matrix and evaluated as one product; per token and predicted layer j the
+ * prediction is that layer's top-k (slot 0 = largest logit, exact ties to
+ * the lower index) with the softmax over the K selected logits.  The walk
+ * j = 1, 2, ..., p continues while every predicted expert of layer l+j is
+ * in the expert cache and stops at the first layer with a missing one: its
+ * missing experts are the ones to preload. */
+typedef struct moe_predictor* moe_predictor_t;
+
+/* Create a predictor for p = n_ahead layers ahead (1..8).
+ *  d_model     multiple of 64, <= 16384;  n_experts 1..64;
+ *  top_k       1..min(8, n_experts);  max_tokens 1..8192
+ *  w_router_next  host array of n_ahead device pointers, each fp16
+ *              [n_experts, d_model] (16-byte aligned): the gates of layers
+ *              l+1 .. l+n_ahead.  They are copied ("stacked") into one
+ *              library-owned array, so they need not outlive the call.
+ * Synchronises `stream`.  *out receives the handle. */
+moe_status moe_predictor_init(int32_t d_model, int32_t n_experts, int32_t top_k,
+                              int32_t n_ahead, int32_t max_tokens,
+                              const void* const* w_router_next, void* stream,
+                              moe_predictor_t* out);
+
+/* Predict for 1 <= n_tokens <= max_tokens tokens (one kernel launch).
+ *  x           device fp16 [n_tokens, d_model]: the current gating input
+ *  cached      device uint64 [n_ahead]: bit e of cached[j-1] set when
+ *              expert e of layer l+j is in the expert cache
+ *  pred_idx    device int32 [n_tokens, n_ahead, top_k]: predicted experts
+ *  pred_w      device fp32 [n_tokens, n_ahead, top_k] or NULL: their
+ *              normalised gate values
+ *  first_miss  device int32 [1]: the first j in 1..n_ahead with a predicted
+ *              expert not cached, 0 if every prediction is cached
+ *  preload     device uint64 [1]: bitmask of the predicted experts of
+ *              layer l+first_miss that are not cached (0 if none) */
+moe_status moe_predict(moe_predictor_t pred, int32_t n_tokens, const void* x,
+                       const uint64_t* cached, int32_t* pred_idx, float* pred_w,
+                       int32_t* first_miss, uint64_t* preload, void* stream);
+
+/* Free the predictor (synchronises the device first). */
+moe_status moe_predictor_destroy(moe_predictor_t pred);
+
 /* Thread-local text of the last error on this thread ("" if none). */
 const char* moe_last_error(void);
 

@@ -22,6 +22,7 @@ EXPORTED = (
     "moe_decode_step_residual", "moe_prefill", "moe_prefill_residual",
     "moe_export_packed", "moe_quantize", "moe_layer_enable_timing",
     "moe_layer_stage_times", "moe_layer_destroy", "moe_last_error",
+    "moe_predictor_init", "moe_predict", "moe_predictor_destroy",
 )
 
 
@@ -215,5 +216,47 @@ class MoeLayer:
         try:
             if getattr(self, "_h", None) is not None and self._h.value:
                 lib().moe_layer_destroy(self._h)
+        except Exception:
+            pass
+
+
+class MoePredictor:
+    """Stacking Computer handle: the gates of the next p layers (a list of p
+    fp16 device tensors [E, d], copied into one stacked array at creation)."""
+
+    def __init__(self, d_model, n_experts, top_k, max_tokens, w_router_next, stream=None):
+        import torch
+        self.d, self.E, self.K, self.p = d_model, n_experts, top_k, len(w_router_next)
+        self.max_tokens = max_tokens
+        arr = ctypes.c_void_p * self.p
+        gates = arr(*[_ptr(w, torch.float16, (n_experts, d_model), "w_router_next").value
+                      for w in w_router_next])
+        h = ctypes.c_void_p()
+        _check(lib().moe_predictor_init(d_model, n_experts, top_k, self.p, max_tokens,
+                                        gates, _stream(stream), ctypes.byref(h)))
+        self._h = h
+
+    def predict(self, x, cached, pred_idx, first_miss, preload, pred_w=None, stream=None):
+        """x [T, d] fp16; cached int64 [p] (bit masks); pred_idx int32 [T, p, K];
+        first_miss int32 [1]; preload int64 [1]; pred_w fp32 [T, p, K] or None."""
+        import torch
+        T = x.shape[0]
+        _check(lib().moe_predict(
+            self._h, T, _ptr(x, torch.float16, (T, self.d), "x"),
+            _ptr(cached, torch.int64, (self.p,), "cached"),
+            _ptr(pred_idx, torch.int32, (T, self.p, self.K), "pred_idx"),
+            _ptr(pred_w, torch.float32, (T, self.p, self.K), "pred_w"),
+            _ptr(first_miss, torch.int32, (1,), "first_miss"),
+            _ptr(preload, torch.int64, (1,), "preload"), _stream(stream)))
+
+    def destroy(self):
+        if self._h is not None and self._h.value:
+            _check(lib().moe_predictor_destroy(self._h))
+        self._h = None
+
+    def __del__(self):
+        try:
+            if getattr(self, "_h", None) is not None and self._h.value:
+                lib().moe_predictor_destroy(self._h)
         except Exception:
             pass

@@ -246,9 +246,145 @@ void free_layer(moe_layer* l) {
 
 }  // namespace
 
+// Stacking Computer handle: the stacked gates of the next p layers and the
+// workspace of one prediction.
+struct moe_predictor {
+  int device = -1;
+  int32_t d = 0, E = 0, K = 0, p = 0, max_tokens = 0;
+  void* arena = nullptr;
+  f16* d_stack = nullptr;        // [p*E, d]
+  float* d_logits = nullptr;     // [max_tokens, p*E]
+  unsigned* d_counter = nullptr; // finished blocks of the running launch
+};
+
+namespace {
+
+std::set<moe_predictor*> g_live_pred;
+
+bool live_pred(moe_predictor* q) {
+  std::lock_guard<std::mutex> g(g_mu);
+  return g_live_pred.count(q) != 0;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* moe_last_error(void) { return g_err.c_str(); }
+
+moe_status moe_predictor_init(int32_t d_model, int32_t n_experts, int32_t top_k,
+                              int32_t n_ahead, int32_t max_tokens,
+                              const void* const* w_router_next, void* stream,
+                              moe_predictor_t* out) {
+  g_err.clear();
+  if (!out) return fail(MOE_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (d_model <= 0 || d_model % 64 || d_model > 16384)
+    return fail(MOE_EINVAL, "d_model must be a positive multiple of 64, <= 16384 (got %d)", d_model);
+  if (n_experts < 1 || n_experts > kMaxExperts)
+    return fail(MOE_EINVAL, "n_experts must be in [1, 64] (got %d)", n_experts);
+  if (top_k < 1 || top_k > kMaxTopK || top_k > n_experts)
+    return fail(MOE_EINVAL, "top_k must be in [1, min(8, n_experts)] (got %d)", top_k);
+  if (n_ahead < 1 || n_ahead > kMaxPredLayers)
+    return fail(MOE_EINVAL, "n_ahead must be in [1, %d] (got %d)", kMaxPredLayers, n_ahead);
+  if (max_tokens < 1 || max_tokens > 8192)
+    return fail(MOE_EINVAL, "max_tokens must be in [1, 8192] (got %d)", max_tokens);
+  if (!w_router_next) return fail(MOE_EINVAL, "w_router_next is NULL");
+  for (int j = 0; j < n_ahead; ++j) {
+    if (!w_router_next[j]) return fail(MOE_EINVAL, "gate %d is NULL", j);
+    if (!aligned16(w_router_next[j])) return fail(MOE_EINVAL, "gate %d must be 16-byte aligned", j);
+  }
+  moe_predictor* q = new (std::nothrow) moe_predictor();
+  if (!q) return fail(MOE_ENOMEM, "host allocation failed");
+  q->d = d_model;
+  q->E = n_experts;
+  q->K = top_k;
+  q->p = n_ahead;
+  q->max_tokens = max_tokens;
+  hipError_t he = hipGetDevice(&q->device);
+  if (he != hipSuccess) { delete q; return hip_fail(he, "hipGetDevice"); }
+  auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  const size_t rows = (size_t)n_ahead * n_experts;
+  const size_t gate_bytes = (size_t)n_experts * d_model * sizeof(f16);
+  const size_t o_stack = 0;
+  const size_t o_logits = o_stack + al(rows * d_model * sizeof(f16));
+  const size_t o_counter = o_logits + al((size_t)max_tokens * rows * sizeof(float));
+  const size_t total = o_counter + al(sizeof(unsigned));
+  he = hipMalloc(&q->arena, total);
+  if (he != hipSuccess) {
+    delete q;
+    return fail(MOE_ENOMEM, "hipMalloc of %zu predictor bytes failed: %s", total, hipGetErrorString(he));
+  }
+  char* base = static_cast<char*>(q->arena);
+  q->d_stack = reinterpret_cast<f16*>(base + o_stack);
+  q->d_logits = reinterpret_cast<float*>(base + o_logits);
+  q->d_counter = reinterpret_cast<unsigned*>(base + o_counter);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the stacking: gate j occupies rows [j*E, (j+1)*E)
+  for (int j = 0; j < n_ahead && he == hipSuccess; ++j)
+    he = hipMemcpyAsync(reinterpret_cast<char*>(q->d_stack) + j * gate_bytes, w_router_next[j],
+                        gate_bytes, hipMemcpyDeviceToDevice, s);
+  if (he == hipSuccess) he = hipMemsetAsync(q->d_counter, 0, sizeof(unsigned), s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
+  if (he != hipSuccess) {
+    (void)hipFree(q->arena);
+    delete q;
+    return hip_fail(he, "predictor init copy");
+  }
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    g_live_pred.insert(q);
+  }
+  *out = q;
+  return MOE_OK;
+}
+
+moe_status moe_predict(moe_predictor_t q, int32_t n_tokens, const void* x,
+                       const uint64_t* cached, int32_t* pred_idx, float* pred_w,
+                       int32_t* first_miss, uint64_t* preload, void* stream) {
+  g_err.clear();
+  if (!q || !live_pred(q)) return fail(MOE_ESTATE, "invalid or destroyed predictor handle");
+  if (n_tokens < 1 || n_tokens > q->max_tokens)
+    return fail(MOE_EINVAL, "n_tokens must be in [1, %d] (got %d)", q->max_tokens, n_tokens);
+  if (!x || !cached || !pred_idx || !first_miss || !preload)
+    return fail(MOE_EINVAL, "x, cached, pred_idx, first_miss and preload must not be NULL");
+  if (!aligned16(x)) return fail(MOE_EINVAL, "x must be 16-byte aligned");
+  if (((uintptr_t)cached & 7u) || ((uintptr_t)preload & 7u))
+    return fail(MOE_EINVAL, "cached and preload must be 8-byte aligned");
+  HIP_TRY(hipSetDevice(q->device), "hipSetDevice");
+  PredictParams pp;
+  pp.x = static_cast<const f16*>(x);
+  pp.wstack = q->d_stack;
+  pp.cached = cached;
+  pp.logits = q->d_logits;
+  pp.counter = q->d_counter;
+  pp.idx = pred_idx;
+  pp.w = pred_w;
+  pp.first_miss = first_miss;
+  pp.preload = preload;
+  pp.T = n_tokens;
+  pp.d = q->d;
+  pp.E = q->E;
+  pp.K = q->K;
+  pp.p = q->p;
+  HIP_TRY(launch_predict(pp, static_cast<hipStream_t>(stream)), "predict kernel launch");
+  return MOE_OK;
+}
+
+moe_status moe_predictor_destroy(moe_predictor_t q) {
+  g_err.clear();
+  if (!q) return fail(MOE_EINVAL, "predictor is NULL");
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    if (!g_live_pred.erase(q)) return fail(MOE_ESTATE, "invalid or destroyed predictor handle");
+  }
+  hipError_t he = hipSetDevice(q->device);
+  if (he == hipSuccess) he = hipDeviceSynchronize();
+  (void)hipFree(q->arena);
+  delete q;
+  if (he != hipSuccess) return hip_fail(he, "destroy synchronize");
+  return MOE_OK;
+}
 
 moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
                           const void* const* w1, const void* const* w3,

@@ -71,6 +71,23 @@ struct RouteParams {
   float t1, t2;
 };
 
+// Stacking Computer (predict.hip): the gates of the next p layers stacked
+// as wstack [p*E, d], applied to the current gating input x [T, d].
+constexpr int kMaxPredLayers = 8;
+
+struct PredictParams {
+  const f16* x;                 // [T, d]
+  const f16* wstack;            // [p*E, d]
+  const uint64_t* cached;       // [p] expert-cache bitmask per predicted layer
+  float* logits;                // [T, p*E] workspace
+  unsigned* counter;            // blocks finished (zero between launches)
+  int32_t* idx;                 // [T, p, K]
+  float* w;                     // [T, p, K] or null
+  int32_t* first_miss;          // [1]
+  uint64_t* preload;            // [1]
+  int32_t T, d, E, K, p;
+};
+
 // ---- launchers (defined in the .hip files) -------------------------------
 hipError_t launch_quantize(const f16* w, int64_t rows, int64_t cols, int bits,
                            uint8_t* codes, f16* scales, hipStream_t s);
@@ -94,6 +111,7 @@ hipError_t launch_decode_up_mfma(const ExpertEntry* table, const WorkList* wl,
 hipError_t launch_decode_down_mfma(const ExpertEntry* table, const WorkList* wl,
                                    const int32_t* perm, const f16* h, float* e_perm,
                                    int d, int f, int max_groups, hipStream_t s);
+hipError_t launch_predict(const PredictParams& q, hipStream_t s);
 hipError_t launch_rmsnorm(const float* h_res, f16* x_next, int T, int d,
                           float eps, hipStream_t s);
 hipError_t launch_prefill_up(const ExpertEntry* table, const WorkList* wl,

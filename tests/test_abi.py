@@ -117,3 +117,36 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         B.lib()
+
+
+def test_predictor_rejects_bad_args():
+    L = B.lib()
+    g = (ctypes.c_void_p * 8)(*([0x1000] * 8))
+    out = ctypes.c_void_p(123)
+    ok = dict(d=256, E=8, K=2, p=3, T=4)
+
+    def init(d=256, E=8, K=2, p=3, T=4, gates=g):
+        return L.moe_predictor_init(d, E, K, p, T, gates, None, ctypes.byref(out))
+
+    for bad in [dict(d=100), dict(d=0), dict(E=0), dict(E=65), dict(K=0), dict(K=9),
+                dict(K=9, E=8), dict(p=0), dict(p=9), dict(T=0), dict(T=9000)]:
+        kw = dict(ok)
+        kw.update(bad)
+        assert init(**kw) == B.MOE_EINVAL, bad
+        assert out.value is None
+    assert init(gates=None) == B.MOE_EINVAL
+    nul = (ctypes.c_void_p * 3)(0x1000, 0, 0x1000)
+    assert init(gates=nul) == B.MOE_EINVAL
+    mis = (ctypes.c_void_p * 3)(0x1000, 0x1008, 0x1000)
+    assert init(gates=mis) == B.MOE_EINVAL
+    assert L.moe_predictor_init(256, 8, 2, 3, 4, g, None, None) == B.MOE_EINVAL
+
+
+def test_predictor_invalid_handles_fail_cleanly():
+    L = B.lib()
+    bogus = ctypes.c_void_p(0xdead0)
+    x = ctypes.c_void_p(0x1000)
+    assert L.moe_predict(bogus, 1, x, x, x, None, x, x, None) == B.MOE_ESTATE
+    assert L.moe_predict(None, 1, x, x, x, None, x, x, None) == B.MOE_ESTATE
+    assert L.moe_predictor_destroy(bogus) == B.MOE_ESTATE
+    assert L.moe_predictor_destroy(None) == B.MOE_EINVAL
