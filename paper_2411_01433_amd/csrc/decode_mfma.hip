@@ -132,28 +132,68 @@ __device__ inline void exchange(const WStage<BITS>& w, u32x4& c0, u32x4& c1) {
   }
 }
 
-// 8 int4 codes (one dword, element e at bits 4e) -> f16x8 times scale.
-// Each 16-bit half h becomes h | h << 12 so the nibble pairs sit at bits
-// (0, 16) and (8, 24); 0x6400 | u is 1024 + u.
-__device__ inline f16x8 deq4(uint32_t w, f16x2 s2) {
-  const uint32_t lo = w & 0xFFFFu, hi = w >> 16;
-  const uint32_t z0 = lo | (lo << 12), z1 = hi | (hi << 12);
-  const f16x2 bias = as_h2(0x64086408u);  // 1024 + 8
-  return pack8(as_u32((as_h2((z0 & 0x000F000Fu) | 0x64006400u) - bias) * s2),
-               as_u32((as_h2(((z0 >> 8) & 0x000F000Fu) | 0x64006400u) - bias) * s2),
-               as_u32((as_h2((z1 & 0x000F000Fu) | 0x64006400u) - bias) * s2),
-               as_u32((as_h2(((z1 >> 8) & 0x000F000Fu) | 0x64006400u) - bias) * s2));
+// Dequantisation pairs codes that sit 16 bits apart in a code word, so one
+// and-or (v_bitop3) gives two fp16 halves: a code u whose lowest bit sits at
+// bit p of a half becomes the fp16 2^(10-p) + u exactly when the exponent
+// field is that of 2^(10-p) (0x6400: 1024 + u at p = 0, 0x5400: 64 + u at
+// p = 4 ...).  A packed subtract removes 2^(10-p) + 2^(b-1) and a packed
+// multiply applies the group scale.  The B fragment's 8 k-slots then hold
+// the columns of its codes in pair order, and the A fragment is permuted to
+// match (the reduction order is free):
+//   int4, word e0..e7 (e_j at bits 4j): slots e0 e4 e1 e5 e2 e6 e3 e7
+//   int2, word e0..e15 (e_j at bits 2j), step half H: slots e(4H) e(4H+8)
+//        e(4H+1) e(4H+9) e(4H+2) e(4H+10) e(4H+3) e(4H+11)
+constexpr uint32_t kAndOr = 0xEA;  // v_bitop3 truth table of (a & b) | c
+
+__device__ inline uint32_t pair_bits(uint32_t w, uint32_t mask, uint32_t expo) {
+  return __builtin_amdgcn_bitop3_b32(w, mask, expo, kAndOr);
+}
+__device__ inline uint32_t scaled(uint32_t v, uint32_t bias, f16x2 s2) {
+  return as_u32((as_h2(v) - as_h2(bias)) * s2);
 }
 
-// 8 int2 codes (16 bits, element e at bits 2e) -> f16x8 times scale;
-// z = h | h << 14 puts e_{2k} at bit 4k and e_{2k+1} at 4k + 16.
-__device__ inline f16x8 deq2(uint32_t h, f16x2 s2) {
-  const uint32_t z = h | (h << 14);
-  const f16x2 bias = as_h2(0x64026402u);  // 1024 + 2
-  return pack8(as_u32((as_h2((z & 0x00030003u) | 0x64006400u) - bias) * s2),
-               as_u32((as_h2(((z >> 4) & 0x00030003u) | 0x64006400u) - bias) * s2),
-               as_u32((as_h2(((z >> 8) & 0x00030003u) | 0x64006400u) - bias) * s2),
-               as_u32((as_h2(((z >> 12) & 0x00030003u) | 0x64006400u) - bias) * s2));
+__device__ inline f16x8 deq4(uint32_t w, f16x2 s2) {
+  const uint32_t w8 = w >> 8;
+  return pack8(scaled(pair_bits(w, 0x000F000Fu, 0x64006400u), 0x64086408u, s2),   // 1024 + 8
+               scaled(pair_bits(w, 0x00F000F0u, 0x54005400u), 0x54805480u, s2),   // 64 + 8
+               scaled(pair_bits(w8, 0x000F000Fu, 0x64006400u), 0x64086408u, s2),
+               scaled(pair_bits(w8, 0x00F000F0u, 0x54005400u), 0x54805480u, s2));
+}
+
+// int2 pairs k = 4H .. 4H+3 of a word: code k at bit 2k of each half (k <= 4
+// in place, k >= 5 after a shift by 10).
+template <int H>
+__device__ inline f16x8 deq2(uint32_t w, f16x2 s2) {
+  if (H == 0) {
+    return pack8(scaled(pair_bits(w, 0x00030003u, 0x64006400u), 0x64026402u, s2),   // 1024 + 2
+                 scaled(pair_bits(w, 0x000C000Cu, 0x5C005C00u), 0x5C085C08u, s2),   // 256 + 2
+                 scaled(pair_bits(w, 0x00300030u, 0x54005400u), 0x54205420u, s2),   // 64 + 2
+                 scaled(pair_bits(w, 0x00C000C0u, 0x4C004C00u), 0x4C804C80u, s2));  // 16 + 2
+  } else {
+    const uint32_t w10 = w >> 10;
+    return pack8(scaled(pair_bits(w, 0x03000300u, 0x44004400u), 0x46004600u, s2),   // 4 + 2
+                 scaled(pair_bits(w10, 0x00030003u, 0x64006400u), 0x64026402u, s2),
+                 scaled(pair_bits(w10, 0x000C000Cu, 0x5C005C00u), 0x5C085C08u, s2),
+                 scaled(pair_bits(w10, 0x00300030u, 0x54005400u), 0x54205420u, s2));
+  }
+}
+
+// low halves of (a, b) / high halves of (a, b) as one dword
+__device__ inline uint32_t lo_lo(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x05040100u);
+}
+__device__ inline uint32_t hi_hi(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x07060302u);
+}
+
+// Slot position of element e of an 8-column (int4) or 16-column (int2)
+// block: the layout in which the up-projection stores h for low-precision
+// groups, so that the down-projection's natural-order fragment loads are
+// already permuted.
+template <int BITS>
+__device__ inline int slot_of(int e) {
+  constexpr int kHalfBlock = BITS == 4 ? 4 : 8;
+  return e < kHalfBlock ? 2 * e : 2 * (e - kHalfBlock) + 1;
 }
 
 // Activation fragments of one stage: lane (t, g) holds columns
@@ -163,7 +203,7 @@ template <int BITS> struct AStage {
   f16x8 a[Geo<BITS>::kSteps];
 };
 
-template <int BITS>
+template <int BITS, bool PERM>
 __device__ inline void load_a(const f16* arow, int64_t kk, int64_t ld, AStage<BITS>& a) {
   using GG = Geo<BITS>;
   const int g = (threadIdx.x & 63) >> 4;
@@ -171,9 +211,29 @@ __device__ inline void load_a(const f16* arow, int64_t kk, int64_t ld, AStage<BI
   for (int c = 0; c < 2; ++c) {
     int64_t col = kk + GG::kLaneCols * g + GG::kChunkCols * c;
     if (BITS != 16) col = col + GG::kChunkCols <= ld ? col : 0;
+    constexpr int kH = GG::kSteps / 2;
 #pragma unroll
-    for (int j = 0; j < GG::kSteps / 2; ++j)
-      a.a[c * (GG::kSteps / 2) + j] = *reinterpret_cast<const f16x8*>(arow + col + 8 * j);
+    for (int j = 0; j < kH; ++j)
+      a.a[c * kH + j] = *reinterpret_cast<const f16x8*>(arow + col + 8 * j);
+    if (PERM && BITS == 4) {  // x0..x7 -> x0 x4 x1 x5 x2 x6 x3 x7
+#pragma unroll
+      for (int j = 0; j < kH; ++j) {
+        const u32x4 v = __builtin_bit_cast(u32x4, a.a[c * kH + j]);
+        a.a[c * kH + j] = __builtin_bit_cast(
+            f16x8, u32x4{lo_lo(v[0], v[2]), hi_hi(v[0], v[2]), lo_lo(v[1], v[3]), hi_hi(v[1], v[3])});
+      }
+    }
+    if (PERM && BITS == 2) {  // x0..x15 -> x0 x8 x1 x9 .. x3 x11 | x4 x12 .. x7 x15
+#pragma unroll
+      for (int j = 0; j < kH; j += 2) {
+        const u32x4 v0 = __builtin_bit_cast(u32x4, a.a[c * kH + j]);
+        const u32x4 v1 = __builtin_bit_cast(u32x4, a.a[c * kH + j + 1]);
+        a.a[c * kH + j] = __builtin_bit_cast(
+            f16x8, u32x4{lo_lo(v0[0], v1[0]), hi_hi(v0[0], v1[0]), lo_lo(v0[1], v1[1]), hi_hi(v0[1], v1[1])});
+        a.a[c * kH + j + 1] = __builtin_bit_cast(
+            f16x8, u32x4{lo_lo(v0[2], v1[2]), hi_hi(v0[2], v1[2]), lo_lo(v0[3], v1[3]), hi_hi(v0[3], v1[3])});
+      }
+    }
   }
 }
 
@@ -187,13 +247,16 @@ __device__ inline void chunk_scales(const WStage<BITS>& w, int64_t kk, int64_t l
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const bool ok = kk + GG::kLaneCols * g + GG::kChunkCols * (c + 1) <= ld;
+    // integer splats: a vector-element read of the packed pair went through
+    // scratch memory
+    const uint32_t sp = BITS == 4 ? w.s[0] : w.s[c];
+    const uint32_t lo = __builtin_amdgcn_perm(sp, sp, 0x01000100u);
+    const uint32_t hi = __builtin_amdgcn_perm(sp, sp, 0x03020302u);
     if (BITS == 4) {  // one group per chunk: halves of s[0]
-      const f16 v = as_h2(w.s[0])[c];
-      sc[c][0] = sc[c][1] = ok ? f16x2{v, v} : f16x2{0, 0};
+      sc[c][0] = sc[c][1] = as_h2(ok ? (c == 1 ? hi : lo) : 0u);
     } else {          // two groups per chunk: s[c]
-      const f16x2 p = as_h2(w.s[c]);
-      sc[c][0] = ok ? f16x2{p[0], p[0]} : f16x2{0, 0};
-      sc[c][1] = ok ? f16x2{p[1], p[1]} : f16x2{0, 0};
+      sc[c][0] = as_h2(ok ? lo : 0u);
+      sc[c][1] = as_h2(ok ? hi : 0u);
     }
   }
 }
@@ -220,7 +283,8 @@ __device__ inline void consume(const WStage<BITS> (&w)[NM], const AStage<BITS>& 
           const uint32_t word = c == 0 ? c0[BITS == 4 ? j : j / 2] : c1[BITS == 4 ? j : j / 2];
           f16x8 b;
           if (BITS == 4) b = deq4(word, sc[c][0]);
-          else b = deq2((word >> (16 * (j & 1))) & 0xFFFFu, sc[c][j / 4]);
+          else if (j & 1) b = deq2<1>(word, sc[c][j / 4]);
+          else b = deq2<0>(word, sc[c][j / 4]);
           acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[c * kHalf + j], b, acc[m], 0, 0, 0);
         }
       }
@@ -253,7 +317,7 @@ __device__ inline void tile_gemm(const ExpertEntry& ex, const int (&mats)[NM], i
     const int64_t kk = col(u);
 #pragma unroll
     for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
-    load_a<BITS>(arow, kk, ld, a[u]);
+    load_a<BITS, NM == 2>(arow, kk, ld, a[u]);
   }
   int64_t i0 = 0;
   for (; i0 + D <= nst; i0 += D) {
@@ -263,7 +327,7 @@ __device__ inline void tile_gemm(const ExpertEntry& ex, const int (&mats)[NM], i
       const int64_t kk = col(i0 + u + D);
 #pragma unroll
       for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
-      load_a<BITS>(arow, kk, ld, a[u]);
+      load_a<BITS, NM == 2>(arow, kk, ld, a[u]);
       // keep the ring order: the scheduler would otherwise sink the loads
       // below the products and wait for nearly all of them each round
       __builtin_amdgcn_sched_barrier(0);
@@ -317,7 +381,11 @@ __device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* p
         const int tok = 4 * (l >> 4) + i;
         if (tok < n) {
           const float a = acc[0][i], b = acc[1][i];
-          h[(int64_t)pairs[tok] * f + row] = (f16)(a / (1.0f + expf(-a)) * b);
+          // low-precision groups store h in the down-projection's slot order
+          constexpr int kBlk = BITS == 4 ? 8 : 16;
+          const int64_t hc = BITS == 16 ? row
+                             : (row & ~(int64_t)(kBlk - 1)) + slot_of<BITS>((int)(row & (kBlk - 1)));
+          h[(int64_t)pairs[tok] * f + hc] = (f16)(a / (1.0f + expf(-a)) * b);
         }
       }
     }

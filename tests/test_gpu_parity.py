@@ -235,6 +235,19 @@ def test_token_counts_both_decode_kernels(T):
     _layer_case(wl, wl.fixed_tags, rng.standard_normal((T, 320)).astype(np.float16))
 
 
+def test_reduction_chunks():
+    """Matrix-core decode with the reduction split into chunks: at 12 tokens
+    the staged activations allow 2048 columns per chunk, so d = 4096 gives
+    two up-projection chunks (partials summed before SwiGLU) and f = 3520
+    two down-projection chunks, the second ragged (1472 columns, a partial
+    last int2 stage); every tag kind."""
+    wl = _edge("edge_chunks", 37, 4096, 3520, 5, 2, 12,
+               [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4, C.TAG_MISS_INT2],
+               t1=0.3, t2=0.9)
+    rng = np.random.default_rng(7)
+    _layer_case(wl, wl.fixed_tags, rng.standard_normal((12, 4096)).astype(np.float16))
+
+
 def test_top1():
     wl = _edge("edge_top1", 35, 256, 256, 8, 1, 7, [C.TAG_INT4] * 8)
     rng = np.random.default_rng(6)
