@@ -254,6 +254,180 @@ struct TableRow {
   }
 };
 
+// ---- decode fast path ------------------------------------------------------
+// When the step's activations fit in LDS (T*d*2 <= 64 KiB) and d <= 4096
+// (8 chunks of 512 columns per lane in registers), the gate takes
+// one memory round trip: each wave issues the loads of its expert row (lane
+// l holds columns 512j + 8l .. +7 of chunk j), the block stages x in LDS,
+// and every token's logit is summed over the chunks in the same order as
+// gate_logits, so the logits are bit-identical to the other routers'.
+constexpr int kFastXBytes = 64 * 1024;
+constexpr int kFastChunks = 8;  // 512-column chunks held in registers at once
+
+__device__ void gate_fast(const RouteParams& p, f16* xs, float* lg) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kW = kRouteThreads / 64;
+  const int nch = (p.d + 511) / 512;
+  const int e0 = wave;
+  // first group of chunks of this wave's first expert row, before staging
+  u32x4 b[kFastChunks];
+#pragma unroll
+  for (int j = 0; j < kFastChunks; ++j) {
+    const int c = j * 512 + lane * 8;
+    b[j] = (e0 < p.E && j < nch && c < p.d)
+               ? *reinterpret_cast<const u32x4*>(p.wg + (int64_t)e0 * p.d + c)
+               : u32x4{0, 0, 0, 0};
+  }
+  // stage x [T, d] in LDS
+  const int nvec = p.T * p.d / 8;
+  for (int v = threadIdx.x; v < nvec; v += kRouteThreads)
+    reinterpret_cast<u32x4*>(xs)[v] = reinterpret_cast<const u32x4*>(p.x)[v];
+  __syncthreads();
+  for (int e = e0; e < p.E; e += kW) {
+    if (e != e0) {
+#pragma unroll
+      for (int j = 0; j < kFastChunks; ++j) {
+        const int c = j * 512 + lane * 8;
+        b[j] = (j < nch && c < p.d) ? *reinterpret_cast<const u32x4*>(p.wg + (int64_t)e * p.d + c)
+                                    : u32x4{0, 0, 0, 0};
+      }
+    }
+    for (int t = 0; t < p.T; ++t) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int j = 0; j < kFastChunks; ++j) {
+        const int c = j * 512 + lane * 8;
+        if (j < nch && c < p.d) {
+          const u32x4 xv = *reinterpret_cast<const u32x4*>(xs + (int64_t)t * p.d + c);
+          acc = dot2(xv.x, b[j].x, acc);
+          acc = dot2(xv.y, b[j].y, acc);
+          acc = dot2(xv.z, b[j].z, acc);
+          acc = dot2(xv.w, b[j].w, acc);
+        }
+      }
+      const float v = wave_sum(acc);
+      if (lane == 0) lg[t * p.E + e] = v;
+    }
+  }
+}
+
+// Order-preserving key of a float (larger float, larger key).
+__device__ inline uint32_t float_key(float v) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// top-k, softmax over the selected logits and the Eq. 2 rule for tokens
+// wave, wave + 16, ...: lanes are experts; slot k is the wave maximum of
+// (logit, -index) over the experts not yet taken, so exact ties keep the
+// lower index.  The softmax and the running Eq. 2 score are evaluated in
+// the same order as decide_token.
+__device__ void decide_wave(const RouteParams& p, const float* lg, const int* tags,
+                            RouteOut o, int32_t* s_idx, int8_t* s_prec) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kW = kRouteThreads / 64;
+  for (int t = wave; t < p.T; t += kW) {
+    float v = lane < p.E ? lg[t * p.E + lane] : -__builtin_inff();
+    int sel[kMaxTopK];
+    float ls[kMaxTopK];
+#pragma unroll
+    for (int k = 0; k < kMaxTopK; ++k) {
+      if (k >= p.K) break;
+      uint64_t key = ((uint64_t)float_key(v) << 32) | (uint32_t)(63 - lane);
+      if (lane >= p.E) key = 0;  // never selected (E >= K experts remain)
+#pragma unroll
+      for (int o_ = 32; o_ > 0; o_ >>= 1) {
+        const uint64_t other = __shfl_xor(key, o_, 64);
+        key = other > key ? other : key;
+      }
+      const int e = 63 - (int)(key & 63u);
+      sel[k] = e;
+      ls[k] = __shfl(v, e, 64);
+      if (lane == e) v = -__builtin_inff();
+    }
+    float ex[kMaxTopK];
+    float z = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kMaxTopK; ++k) {
+      if (k < p.K) {
+        ex[k] = expf(ls[k] - ls[0]);
+        z += ex[k];
+      }
+    }
+    float above = 0.0f;  // Eq. 2 running score
+#pragma unroll
+    for (int k = 0; k < kMaxTopK; ++k) {
+      if (k >= p.K) break;
+      const float w = ex[k] / z;
+      const int e = sel[k];
+      const int tag = tags[e];
+      int prec;
+      if (tag == TAG_FP16) {
+        prec = PREC_HIGH;
+      } else if (tag == TAG_INT4 || tag == TAG_INT2) {
+        prec = PREC_LOW;
+      } else {
+        const float sc = (k == 0) ? 0.0f : above;
+        prec = (k == 0 || sc <= p.t1) ? PREC_HIGH : (sc <= p.t2 ? PREC_LOW : PREC_SKIP);
+      }
+      above += w;
+      if (lane == k) {
+        const int pi = t * p.K + k;
+        o.idx[pi] = e;
+        o.w[pi] = w;
+        o.prec[pi] = (int8_t)prec;
+        s_idx[pi] = e;
+        s_prec[pi] = (int8_t)prec;
+        if (o.user_idx) o.user_idx[pi] = e;
+        if (o.user_w) o.user_w[pi] = w;
+        if (o.user_prec) o.user_prec[pi] = (int8_t)prec;
+      }
+    }
+  }
+}
+
+// The stable counting sort of build_worklist for at most 64 pairs, in one
+// wave: keys in increasing order, one ballot each; a pair's rank is the
+// number of lower lanes with the same key.
+__device__ void worklist_wave(const RouteParams& p, const int32_t* idx, const int8_t* prec,
+                              const int* low_bits, WorkList* wl, int32_t* perm, int32_t* pos) {
+  const int lane = threadIdx.x & 63;
+  const int N = p.T * p.K;
+  int key = -1;
+  if (lane < N) {
+    const int pr = prec[lane];
+    if (pr != PREC_SKIP) key = idx[lane] * 2 + (pr == PREC_LOW);
+    else pos[lane] = -1;
+  }
+  const uint64_t lower = (1ull << lane) - 1ull;
+  int off = 0, ng = 0, mx = 0;
+  for (int k = 0; k < 2 * p.E; ++k) {
+    const uint64_t m = __ballot(key == k);
+    if (m == 0) continue;
+    const int c = __popcll(m);
+    if (key == k) {
+      const int at = off + __popcll(m & lower);
+      perm[at] = lane;
+      pos[lane] = at;
+    }
+    if (lane == 0) {
+      Group g;
+      g.expert = k >> 1;
+      g.bits = (k & 1) ? low_bits[k >> 1] : 16;
+      g.offset = off;
+      g.count = c;
+      wl->groups[ng] = g;
+    }
+    ++ng;
+    off += c;
+    mx = c > mx ? c : mx;
+  }
+  if (lane == 0) {
+    wl->n_groups = ng;
+    wl->max_count = mx;
+  }
+}
+
 // Decode: one block routes every token and builds the work list.
 __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
     RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
@@ -261,17 +435,23 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
   __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
   __shared__ int32_t s_idx[kDecodeMaxTokens * kMaxTopK];
   __shared__ int8_t s_prec[kDecodeMaxTokens * kMaxTopK];
+  __shared__ __attribute__((aligned(16))) f16 xs[kFastXBytes / 2];
   TableRow tr;
   tr.load(p);
-  if (p.T == 1) gate_logits<1, 8>(p, 0, p.T, lg);
+  const bool fast = (int64_t)p.T * p.d * 2 <= kFastXBytes && p.d <= kFastChunks * 512;
+  if (fast) gate_fast(p, xs, lg);
+  else if (p.T == 1) gate_logits<1, 8>(p, 0, p.T, lg);
   else if (p.T == 2) gate_logits<2, 8>(p, 0, p.T, lg);
   else gate_logits<4, 4>(p, 0, p.T, lg);
   tr.store(p, tags, low_bits);
   __syncthreads();
-  for (int t = threadIdx.x; t < p.T; t += blockDim.x)
-    decide_token(p, t, lg + t * p.E, tags, o, s_idx, s_prec);
+  decide_wave(p, lg, tags, o, s_idx, s_prec);
   __syncthreads();
-  build_worklist(p, s_idx, s_prec, low_bits, wl, perm, pos);
+  if (p.T * p.K <= 64) {
+    if (threadIdx.x < 64) worklist_wave(p, s_idx, s_prec, low_bits, wl, perm, pos);
+  } else {
+    build_worklist(p, s_idx, s_prec, low_bits, wl, perm, pos);
+  }
 }
 
 // Prefill: many blocks route their tokens; a second kernel builds the list.
