@@ -79,7 +79,7 @@ __device__ inline int perm8(int i) { return i < 4 ? 2 * i : 2 * (i - 4) + 1; }
 // (rows beyond n and columns beyond ld are zero).
 struct ActStager {
   const f16* row[kStageRowsPerThread];
-  u32x4 v[kStageRowsPerThread];
+  u32x4 v[2][kStageRowsPerThread];  // two stages in flight
 
   __device__ void init(const f16* src, int64_t ld, const int32_t* perm, int off,
                        int j0, int n, int K, bool gather) {
@@ -93,18 +93,19 @@ struct ActStager {
       }
     }
   }
+  template <int SLOT>
   __device__ void fetch(int64_t ld, int64_t k0) {
     const int64_t col = k0 + (threadIdx.x % kPieces) * 8;
 #pragma unroll
     for (int i = 0; i < kStageRowsPerThread; ++i)
-      v[i] = (row[i] && col < ld) ? *reinterpret_cast<const u32x4*>(row[i] + col)
-                                  : u32x4{0, 0, 0, 0};
+      v[SLOT][i] = (row[i] && col < ld) ? *reinterpret_cast<const u32x4*>(row[i] + col)
+                                        : u32x4{0, 0, 0, 0};
   }
-  template <bool PERMUTE>
+  template <int SLOT, bool PERMUTE>
   __device__ void store(f16* lds) const {
 #pragma unroll
     for (int i = 0; i < kStageRowsPerThread; ++i) {
-      u32x4 x = v[i];
+      u32x4 x = v[SLOT][i];
       if (PERMUTE) {
         const f16x8 a = __builtin_bit_cast(f16x8, x);
         f16x8 b;
@@ -208,8 +209,10 @@ template <> struct WFrag<2> {
 // One pass (up to kPassTok tokens) of one group over NM matrices:
 // acc[rt][tt][m] accumulates the tokens of tile tt against the weight rows
 // of tile rt.  Software pipeline: while the MFMAs of stage k run, the
-// activations and weight fragments of stage k+1 are already in flight.
-template <int BITS, int NM, int RT>
+// weight fragments of stage k+2 and the activations of stage k+ADEPTH are
+// in flight (ADEPTH 2: two register slots, used by the down-projection; the
+// up-projection's registers are full).
+template <int BITS, int NM, int RT, int ADEPTH>
 __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
                           int64_t wrow0, int64_t n_rows, int64_t ld,
                           const f16* act, int64_t act_ld, const int32_t* perm,
@@ -233,46 +236,95 @@ __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
   };
   ActStager st;
   st.init(act, act_ld, perm, off, j0, n, K, gather);
-  st.fetch(act_ld, 0);
+  st.fetch<0>(act_ld, 0);
   WFrag<BITS> w0[RT][NM], w1[RT][NM];
   load_w(w0, 0);
   load_w(w1, kStageK);   // masked beyond ld
-  int buf = 0;
-  for (int64_t k0 = 0; k0 < ld; k0 += kStageK, buf ^= 1) {
-    f16* cur = lds + buf * (kPassTok * kLdsRow);
-    // the buffer written here was last read two stages ago, before the
-    // previous stage's barrier
-    st.store<BITS != 16>(cur);
-    __syncthreads();
-    if (k0 + kStageK < ld) st.fetch(act_ld, k0 + kStageK);
-    WFrag<BITS> w2[RT][NM];
-    load_w(w2, k0 + 2 * kStageK);
+  if constexpr (ADEPTH == 1) {
+    int buf = 0;
+    for (int64_t k0 = 0; k0 < ld; k0 += kStageK, buf ^= 1) {
+      f16* cur = lds + buf * (kPassTok * kLdsRow);
+      // the buffer written here was last read two stages ago, before the
+      // previous stage's barrier
+      st.store<0, BITS != 16>(cur);
+      __syncthreads();
+      if (k0 + kStageK < ld) st.fetch<0>(act_ld, k0 + kStageK);
+      WFrag<BITS> w2[RT][NM];
+      load_w(w2, k0 + 2 * kStageK);
 #pragma unroll
-    for (int s = 0; s < kSteps; ++s) {
-      f16x8 b[RT][NM];
+      for (int s = 0; s < kSteps; ++s) {
+        f16x8 b[RT][NM];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int m = 0; m < NM; ++m) b[rt][m] = w0[rt][m].get(s);
+#pragma unroll
+        for (int tt = 0; tt < kTokTiles; ++tt) {
+          if (tt < ntile) {
+            const f16x8 a = a_frag<BITS>(cur, tt, s);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+              for (int m = 0; m < NM; ++m)
+                acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[rt][m], acc[rt][tt][m], 0, 0, 0);
+          }
+        }
+      }
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int m = 0; m < NM; ++m) b[rt][m] = w0[rt][m].get(s);
+        for (int m = 0; m < NM; ++m) {
+          w0[rt][m] = w1[rt][m];
+          w1[rt][m] = w2[rt][m];
+        }
+    }
+  } else {
+  st.fetch<1>(act_ld, kStageK);
+  // two stages per iteration: LDS buffers and activation slots alternate
+  for (int64_t k00 = 0; k00 < ld; k00 += 2 * kStageK) {
 #pragma unroll
-      for (int tt = 0; tt < kTokTiles; ++tt) {
-        if (tt < ntile) {
-          const f16x8 a = a_frag<BITS>(cur, tt, s);
+    for (int u = 0; u < 2; ++u) {
+      const int64_t k0 = k00 + u * kStageK;
+      f16* cur = lds + u * (kPassTok * kLdsRow);
+      // the buffer written here was last read two stages ago, before the
+      // previous stage's barrier; its activations were fetched two stages ago
+      if (u == 0) st.store<0, BITS != 16>(cur);
+      else st.store<1, BITS != 16>(cur);
+      __syncthreads();
+      if (u == 0) st.fetch<0>(act_ld, k0 + 2 * kStageK);
+      else st.fetch<1>(act_ld, k0 + 2 * kStageK);
+      WFrag<BITS> w2[RT][NM];
+      load_w(w2, k0 + 2 * kStageK);
+      if (k0 < ld) {
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) {
+          f16x8 b[RT][NM];
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int m = 0; m < NM; ++m)
-              acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[rt][m], acc[rt][tt][m], 0, 0, 0);
+            for (int m = 0; m < NM; ++m) b[rt][m] = w0[rt][m].get(s);
+#pragma unroll
+          for (int tt = 0; tt < kTokTiles; ++tt) {
+            if (tt < ntile) {
+              const f16x8 a = a_frag<BITS>(cur, tt, s);
+#pragma unroll
+              for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int m = 0; m < NM; ++m)
+                  acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[rt][m], acc[rt][tt][m], 0, 0, 0);
+            }
+          }
         }
       }
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+          w0[rt][m] = w1[rt][m];
+          w1[rt][m] = w2[rt][m];
+        }
     }
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int m = 0; m < NM; ++m) {
-        w0[rt][m] = w1[rt][m];
-        w1[rt][m] = w2[rt][m];
-      }
+  }
   }
   __syncthreads();  // the LDS buffers are reused by the next pass
 }
@@ -287,7 +339,7 @@ __device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* p
   for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
     const int n = min(kPassTok, g.count - j0);
     f32x4 acc[RT][kTokTiles][2];
-    gemm_pass<BITS, 2, RT>(ex, mats, wrow0, f, d, x, d, perm, g.offset, j0, n, K, true, lds, acc);
+    gemm_pass<BITS, 2, RT, 1>(ex, mats, wrow0, f, d, x, d, perm, g.offset, j0, n, K, true, lds, acc);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int64_t row = wrow0 + rt * 16 + (l & 15);
@@ -335,7 +387,7 @@ __device__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
   for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
     const int n = min(kPassTok, g.count - j0);
     f32x4 acc[RT][kTokTiles][1];
-    gemm_pass<BITS, 1, RT>(ex, mats, wrow0, d, f, h, f, nullptr, g.offset, j0, n, 1, false, lds, acc);
+    gemm_pass<BITS, 1, RT, 2>(ex, mats, wrow0, d, f, h, f, nullptr, g.offset, j0, n, 1, false, lds, acc);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int64_t row = wrow0 + rt * 16 + (l & 15);
