@@ -416,6 +416,72 @@ def run_predictor(args):
             "results": res}
 
 
+def run_cache(args):
+    """Mixed-precision expert cache manager (Section 3.4): miss penalty of
+    each replacement policy on a seeded Mixtral-shaped synthetic trace, the
+    Eq. 3 weights chosen on a separate calibration trace (grid of step 1/4
+    over the simplex), and the manager's replay rate against the oracle.
+    Host-side mode: no GPU work."""
+    import itertools
+    import numpy as np
+    import paper_2411_01433_amd as P
+    from synth import traces as TR
+    L, E, K = 32, 8, 2
+    hi_cap, lo_cap = L * E // 4, L * E // 8
+    seqs, seq_len = 8, 128
+    cal = TR.expert_trace(7, seqs, seq_len, L, E, K)
+    test = TR.expert_trace(8, seqs, seq_len, L, E, K)
+    n_tok = seqs * seq_len
+
+    def penalty(w, tr):
+        c = P.MoeCache(L, E, hi_cap, lo_cap, *w, bits_hi=16, bits_lo=4, miss_cost=1.0)
+        c.replay(*tr)
+        pen, hm, lm, hits = c.stats()
+        c.destroy()
+        return pen, hm, lm, hits
+
+    grid = [w for w in itertools.product(range(5), repeat=4) if sum(w) == 4]
+    grid = [tuple(v / 4 for v in w) for w in grid]
+    best = min(grid, key=lambda w: (penalty(w, cal)[0], w))
+    res = {}
+    for name, w in (("lru", (1, 0, 0, 0)), ("lfu", (0, 1, 0, 0)), ("lhu", (0, 0, 1, 0)),
+                    ("fld", (0, 0, 0, 1)), ("equal", (0.25,) * 4), ("calibrated", best)):
+        pen, hm, lm, hits = penalty(w, test)
+        res[name] = {"weights": list(w), "penalty_per_token": pen / n_tok,
+                     "hi_misses": hm, "lo_misses": lm, "hits": hits}
+        log(f"{name:10s} w={w} penalty/token {pen / n_tok:.4f} "
+            f"hi-miss {hm} lo-miss {lm} hits {hits}")
+    # replay rate of the library and of the oracle (the oracle on a sample)
+    c = P.MoeCache(L, E, hi_cap, lo_cap, *best, bits_hi=16, bits_lo=4)
+    t0 = time.perf_counter()
+    reps = 20
+    for _ in range(reps):
+        c.replay(*test)
+    lib_s = (time.perf_counter() - t0) / reps
+    c.destroy()
+    n_uses = len(test[0])
+    out = {"metric": "expert-cache miss penalty per token (C units) and manager uses/s",
+           "unit": "uses/s", "value": n_uses / lib_s, "higher_is_better": True,
+           "data": "synthetic", "dtype": "f64",
+           "config": {"workload": "mixtral_shaped_cache_trace", "n_layers": L, "n_experts": E,
+                      "top_k": K, "hi_capacity": hi_cap, "lo_capacity": lo_cap,
+                      "sequences": seqs, "tokens_per_sequence": seq_len, "uses": n_uses,
+                      "bits_hi": 16, "bits_lo": 4},
+           "policies": res, "us_per_token": lib_s / n_tok * 1e6}
+    if not args.no_cpu_baseline:
+        from oracle import cache_oracle as CO
+        cfg = CO.CacheConfig(L, E, hi_cap, lo_cap, *best, bits_hi=16, bits_lo=4)
+        m = min(n_uses, 20000)
+        sample = [tuple(int(a[i]) for a in test[:4]) for i in range(m)]
+        t0 = time.perf_counter()
+        CO.replay(cfg, sample, sequence_starts=[0])
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": m / dt, "unit": "uses/s", "cores": 1, "kind": "oracle",
+                               "sample": f"first {m} uses of the same trace, Python oracle",
+                               "seconds": dt}
+    return out
+
+
 def parity_and_cpu(args, state, out):
     """Check sampled steps against the oracle and time the oracle itself."""
     import torch
@@ -490,7 +556,12 @@ def main():
                     help="plain 256 MiB device copy x5 (counter calibration)")
     ap.add_argument("--predictor", action="store_true",
                     help="time the Stacking Computer against sequential gates, p = 1..8")
+    ap.add_argument("--cache", action="store_true",
+                    help="expert cache manager: policy miss penalties and replay rate (host only)")
     args = ap.parse_args()
+    if args.cache:
+        print(json.dumps(run_cache(args)), flush=True)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this library runs the layer on a "
               "single MI355X (no multi-GPU path); run with --gpus 1.", file=sys.stderr)

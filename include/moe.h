@@ -231,6 +231,84 @@ moe_status moe_predict(moe_predictor_t pred, int32_t n_tokens, const void* x,
 /* Free the predictor (synchronises the device first). */
 moe_status moe_predictor_destroy(moe_predictor_t pred);
 
+/* ---- Mixed-precision expert cache manager ---------------------------------
+ * Section 3.4 ("Cache Manager design", Eq. 3) and "Cache replacement
+ * policies".  Host-side bookkeeping that decides which expert copies stay
+ * resident; layer_tags() turns its state into the per-expert tags of
+ * moe_set_expert_precision.  No GPU work, no HIP calls.
+ *
+ * Experts are (layer, expert) pairs.  Two caches hold high- and
+ * low-precision copies (capacities counted in experts).  Per sequence the
+ * manager records for every expert t its last-use time R_t (token number),
+ * use count F_t and high-precision use count H_t (low-precision uses do not
+ * count in H_t); uses update the records whether they hit or miss.  A use
+ * names the copy (high or low) and hits when that copy is resident; on a
+ * miss the copy is inserted, and when its cache is full the resident with
+ * the lowest priority (Eq. 3)
+ *   p_t = w_lru R_t/T + w_lfu F_t/T + w_lhu H_t/T
+ *         + w_fld (1 - ((l_t - l_i + n_layers) mod n_layers) / n_layers)
+ * is evicted: T is the current token number (the three record terms are 0
+ * before the first token), l_i the layer of the incoming copy; ties evict
+ * the smaller key layer * n_experts + expert; residents masked by the
+ * expert predictor (Section 3.3) are kept unless every resident is masked.
+ * A high-precision miss adds miss_cost to the penalty, a low-precision miss
+ * miss_cost * bits_lo / bits_hi.
+ * One handle is not safe for concurrent use from several threads. */
+typedef struct moe_cache* moe_cache_t;
+
+typedef struct {
+  int32_t n_layers, n_experts;     /* >= 1 each, product <= 2^24 */
+  int32_t hi_capacity, lo_capacity;/* >= 0 (0: that cache holds nothing) */
+  double w_lru, w_lfu, w_lhu, w_fld;  /* >= 0, sum 1 (within 1e-6) */
+  int32_t bits_hi, bits_lo;        /* 1 <= bits_lo <= bits_hi (e.g. 16 / 4) */
+  double miss_cost;                /* C: cost of one high-precision miss, >= 0 */
+} moe_cache_desc;
+
+/* Create an empty cache manager; *out receives the handle. */
+moe_status moe_cache_create(const moe_cache_desc* desc, moe_cache_t* out);
+
+/* A new sequence: T = 0 and the R, F, H records restart; contents stay. */
+moe_status moe_cache_begin_sequence(moe_cache_t cache);
+
+/* The next token: T += 1 (tokens are numbered 1, 2, ... per sequence). */
+moe_status moe_cache_begin_token(moe_cache_t cache);
+
+/* One use of expert (layer, expert) through its high (high != 0) or low
+ * copy.  *hit (if non-NULL) = 1 when that copy was resident; the evicted
+ * expert (or -1, -1) goes to *evicted_layer / *evicted_expert (non-NULL). */
+moe_status moe_cache_access(moe_cache_t cache, int32_t layer, int32_t expert, int32_t high,
+                            int32_t* hit, int32_t* evicted_layer, int32_t* evicted_expert);
+
+/* *present = 1 when the high (high != 0) or low copy is resident. */
+moe_status moe_cache_contains(moe_cache_t cache, int32_t layer, int32_t expert, int32_t high,
+                              int32_t* present);
+
+/* Mask (masked != 0) or unmask an expert against eviction (predicted
+ * experts, Section 3.3); clear_masks unmasks all. */
+moe_status moe_cache_set_mask(moe_cache_t cache, int32_t layer, int32_t expert, int32_t masked);
+moe_status moe_cache_clear_masks(moe_cache_t cache);
+
+/* Replay n uses (host arrays of n entries): the token number advances
+ * whenever tokens[i] differs from the previous use's, and a new sequence
+ * starts before use i when new_sequence (may be NULL) has new_sequence[i]
+ * != 0.  hits[i] (may be NULL) = 1 for a hit; evicted[i] (may be NULL) =
+ * evicted key layer * n_experts + expert or -1.  All indices are checked
+ * before any use is applied. */
+moe_status moe_cache_replay(moe_cache_t cache, int64_t n, const int32_t* tokens,
+                            const int32_t* layers, const int32_t* experts, const int32_t* highs,
+                            const uint8_t* new_sequence, int32_t* hits, int32_t* evicted);
+
+/* Tags of the n_experts experts of one layer (host int32 array): FP16 when
+ * the high copy is resident, else MISS_INT4 / MISS_INT2 (bits_lo 4 / 2;
+ * other widths: MOE_EUNSUPPORTED) so that the Eq. 2 rule decides per token. */
+moe_status moe_cache_layer_tags(moe_cache_t cache, int32_t layer, int32_t* tags);
+
+/* Accumulated miss penalty and counts since creation (NULL outputs skipped). */
+moe_status moe_cache_stats(moe_cache_t cache, double* penalty, int64_t* hi_misses,
+                           int64_t* lo_misses, int64_t* hits);
+
+moe_status moe_cache_destroy(moe_cache_t cache);
+
 /* Thread-local text of the last error on this thread ("" if none). */
 const char* moe_last_error(void);
 

@@ -23,6 +23,10 @@ EXPORTED = (
     "moe_export_packed", "moe_quantize", "moe_layer_enable_timing",
     "moe_layer_stage_times", "moe_layer_destroy", "moe_last_error",
     "moe_predictor_init", "moe_predict", "moe_predictor_destroy",
+    "moe_cache_create", "moe_cache_begin_sequence", "moe_cache_begin_token",
+    "moe_cache_access", "moe_cache_contains", "moe_cache_set_mask",
+    "moe_cache_clear_masks", "moe_cache_replay", "moe_cache_layer_tags",
+    "moe_cache_stats", "moe_cache_destroy",
 )
 
 
@@ -39,6 +43,17 @@ class LayerDesc(ctypes.Structure):
         ("group_size", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
         ("t1", ctypes.c_float), ("t2", ctypes.c_float),
         ("rms_eps", ctypes.c_float), ("flags", ctypes.c_uint32),
+    ]
+
+
+class CacheDesc(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("n_experts", ctypes.c_int32),
+        ("hi_capacity", ctypes.c_int32), ("lo_capacity", ctypes.c_int32),
+        ("w_lru", ctypes.c_double), ("w_lfu", ctypes.c_double),
+        ("w_lhu", ctypes.c_double), ("w_fld", ctypes.c_double),
+        ("bits_hi", ctypes.c_int32), ("bits_lo", ctypes.c_int32),
+        ("miss_cost", ctypes.c_double),
     ]
 
 
@@ -70,6 +85,21 @@ def lib() -> ctypes.CDLL:
     L.moe_layer_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int32)]
     L.moe_layer_destroy.argtypes = [vp]
+    pi32 = ctypes.POINTER(ctypes.c_int32)
+    L.moe_cache_create.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(vp)]
+    L.moe_cache_begin_sequence.argtypes = [vp]
+    L.moe_cache_begin_token.argtypes = [vp]
+    L.moe_cache_access.argtypes = [vp, i32, i32, i32, pi32, pi32, pi32]
+    L.moe_cache_contains.argtypes = [vp, i32, i32, i32, pi32]
+    L.moe_cache_set_mask.argtypes = [vp, i32, i32, i32]
+    L.moe_cache_clear_masks.argtypes = [vp]
+    L.moe_cache_replay.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp]
+    L.moe_cache_layer_tags.argtypes = [vp, i32, pi32]
+    L.moe_cache_stats.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_int64)]
+    L.moe_cache_destroy.argtypes = [vp]
     L.moe_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
         if name != "moe_last_error":
@@ -258,5 +288,89 @@ class MoePredictor:
         try:
             if getattr(self, "_h", None) is not None and self._h.value:
                 lib().moe_predictor_destroy(self._h)
+        except Exception:
+            pass
+
+
+class MoeCache:
+    """Mixed-precision expert cache manager (host side, no device work)."""
+
+    def __init__(self, n_layers, n_experts, hi_capacity, lo_capacity, w_lru, w_lfu, w_lhu,
+                 w_fld, bits_hi=16, bits_lo=4, miss_cost=1.0):
+        self.n_layers, self.n_experts = n_layers, n_experts
+        desc = CacheDesc(n_layers, n_experts, hi_capacity, lo_capacity, w_lru, w_lfu, w_lhu,
+                         w_fld, bits_hi, bits_lo, miss_cost)
+        h = ctypes.c_void_p()
+        _check(lib().moe_cache_create(ctypes.byref(desc), ctypes.byref(h)))
+        self._h = h
+
+    def begin_sequence(self):
+        _check(lib().moe_cache_begin_sequence(self._h))
+
+    def begin_token(self):
+        _check(lib().moe_cache_begin_token(self._h))
+
+    def access(self, layer, expert, high):
+        """(hit, evicted (layer, expert) or None)."""
+        hit, el, ee = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().moe_cache_access(self._h, layer, expert, 1 if high else 0,
+                                      ctypes.byref(hit), ctypes.byref(el), ctypes.byref(ee)))
+        return bool(hit.value), (None if el.value < 0 else (el.value, ee.value))
+
+    def contains(self, layer, expert, high):
+        v = ctypes.c_int32()
+        _check(lib().moe_cache_contains(self._h, layer, expert, 1 if high else 0,
+                                        ctypes.byref(v)))
+        return bool(v.value)
+
+    def set_mask(self, layer, expert, masked):
+        _check(lib().moe_cache_set_mask(self._h, layer, expert, 1 if masked else 0))
+
+    def clear_masks(self):
+        _check(lib().moe_cache_clear_masks(self._h))
+
+    def replay(self, tokens, layers, experts, highs, new_sequence=None):
+        """Replay a trace (numpy arrays); returns (hits int32 [n], evicted int32 [n],
+        key layer * n_experts + expert or -1)."""
+        import numpy as np
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        n = t.shape[0]
+        arrs = [np.ascontiguousarray(a, dtype=np.int32) for a in (layers, experts, highs)]
+        if any(a.shape != (n,) for a in arrs):
+            raise ValueError("trace arrays must have the same length")
+        ns = None if new_sequence is None else np.ascontiguousarray(new_sequence, dtype=np.uint8)
+        if ns is not None and ns.shape != (n,):
+            raise ValueError("new_sequence must have the trace's length")
+        hits = np.empty(n, np.int32)
+        ev = np.empty(n, np.int32)
+        p = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+        _check(lib().moe_cache_replay(self._h, n, p(t), p(arrs[0]), p(arrs[1]), p(arrs[2]),
+                                      p(ns), p(hits), p(ev)))
+        return hits, ev
+
+    def layer_tags(self, layer):
+        import numpy as np
+        tags = np.empty(self.n_experts, np.int32)
+        _check(lib().moe_cache_layer_tags(self._h, layer,
+                                          tags.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
+        return tags
+
+    def stats(self):
+        """(penalty, hi_misses, lo_misses, hits)."""
+        pen = ctypes.c_double()
+        a, b, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().moe_cache_stats(self._h, ctypes.byref(pen), ctypes.byref(a),
+                                     ctypes.byref(b), ctypes.byref(c)))
+        return pen.value, a.value, b.value, c.value
+
+    def destroy(self):
+        if self._h is not None and self._h.value:
+            _check(lib().moe_cache_destroy(self._h))
+        self._h = None
+
+    def __del__(self):
+        try:
+            if getattr(self, "_h", None) is not None and self._h.value:
+                lib().moe_cache_destroy(self._h)
         except Exception:
             pass

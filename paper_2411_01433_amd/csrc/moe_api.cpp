@@ -268,6 +268,10 @@ bool live_pred(moe_predictor* q) {
 
 }  // namespace
 
+namespace moe {
+void set_last_error(const char* msg) { g_err = msg; }
+}  // namespace moe
+
 extern "C" {
 
 const char* moe_last_error(void) { return g_err.c_str(); }
