@@ -187,6 +187,56 @@ moe_status moe_layer_stage_times(moe_layer_t layer, double* ms,
  * the device first).  The borrowed fp16 weights are not touched. */
 moe_status moe_layer_destroy(moe_layer_t layer);
 
+/* ---- Expert storage and loading (Dynamic Expert Loader) ---------------
+ * Section 3.1 and Fig. 4: expert copies live in host Expert Storage and a
+ * cache miss loads the copy of the precision the Eq. 2 rule chose into the
+ * GPU expert cache; Section 2.2: an int4 copy loads up to 4x faster than
+ * the fp16 expert.  A store keeps one layer's experts in pinned host memory
+ * (hipHostMalloc): fp16 W1, W3 [d_ff, d_model], W2 [d_model, d_ff] and
+ * their low_bits copy (codes + fp16 group scales, the same quantiser and
+ * layout as moe_quantize).  Loads are hipMemcpyAsync transfers on the
+ * caller's stream into caller-owned device buffers ("cache slots");
+ * moe_layer_bind_expert points a layer's expert at such slots. */
+typedef struct moe_store* moe_store_t;
+
+/* d_model, d_ff: positive multiples of 64 (<= 16384 / 65536); n_experts
+ * 1..64; low_bits 4 or 2.  Allocates the pinned storage on the current
+ * device (MOE_ENOMEM if it cannot). */
+moe_status moe_store_create(int32_t d_model, int32_t d_ff, int32_t n_experts,
+                            int32_t low_bits, moe_store_t* out);
+
+/* Bytes of one matrix's fp16 weights, low-precision codes and scales (the
+ * three matrices of an expert have equal sizes). */
+moe_status moe_store_sizes(moe_store_t store, int64_t* fp16_bytes, int64_t* code_bytes,
+                           int64_t* scale_bytes);
+
+/* Fill expert `expert` from device fp16 weights (16-byte aligned): copies
+ * them to the host and quantises them on the device into the host low
+ * copy.  Synchronises `stream`. */
+moe_status moe_store_put(moe_store_t store, int32_t expert, const void* w1, const void* w3,
+                         const void* w2, void* stream);
+
+/* Asynchronous load on `stream` of expert `expert`'s fp16 matrices
+ * (high != 0: dst_w[3], fp16_bytes each) or low copy (dst_q[3] code_bytes,
+ * dst_s[3] scale_bytes each) into device buffers.  MOE_ESTATE if the expert
+ * was never put. */
+moe_status moe_store_load(moe_store_t store, int32_t expert, int32_t high, void* const* dst_w,
+                          void* const* dst_q, void* const* dst_s, void* stream);
+
+/* Free the pinned storage (synchronises the device first). */
+moe_status moe_store_destroy(moe_store_t store);
+
+/* Point expert `expert` of a layer at caller-owned device copies (borrowed:
+ * they must outlive their use), in stream order on `stream`: tag FP16
+ * needs w[3] (fp16, layout as moe_layer_init); INT4 / INT2 need q[3], s[3]
+ * with low_bits 4 / 2 (layout as moe_quantize); MISS_INT4 / MISS_INT2 need
+ * all of them.  Pointers must be 16-byte aligned.  An expert bound without
+ * fp16 weights cannot take moe_set_expert_precision (MOE_ESTATE) until it
+ * is bound again; moe_export_packed reports only library-built copies. */
+moe_status moe_layer_bind_expert(moe_layer_t layer, int32_t expert, int32_t tag,
+                                 const void* const* w, const void* const* q,
+                                 const void* const* s, int32_t low_bits, void* stream);
+
 /* ---- Stacking Computer of the Adaptive Expert Predictor ----------------
  * Section 3.3 ("Expert predictor design") and Fig. 7: gating inputs of
  * consecutive layers are similar, so the gates of the next p layers

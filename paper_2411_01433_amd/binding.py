@@ -27,6 +27,8 @@ EXPORTED = (
     "moe_cache_access", "moe_cache_contains", "moe_cache_set_mask",
     "moe_cache_clear_masks", "moe_cache_replay", "moe_cache_layer_tags",
     "moe_cache_stats", "moe_cache_destroy",
+    "moe_store_create", "moe_store_sizes", "moe_store_put", "moe_store_load",
+    "moe_store_destroy", "moe_layer_bind_expert",
 )
 
 
@@ -100,6 +102,15 @@ def lib() -> ctypes.CDLL:
                                   ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_int64)]
     L.moe_cache_destroy.argtypes = [vp]
+    L.moe_store_create.argtypes = [i32, i32, i32, i32, ctypes.POINTER(vp)]
+    L.moe_store_sizes.argtypes = [vp, ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
+    L.moe_store_put.argtypes = [vp, i32, vp, vp, vp, vp]
+    L.moe_store_load.argtypes = [vp, i32, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                 ctypes.POINTER(vp), vp]
+    L.moe_store_destroy.argtypes = [vp]
+    L.moe_layer_bind_expert.argtypes = [vp, i32, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                        ctypes.POINTER(vp), i32, vp]
     L.moe_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
         if name != "moe_last_error":
@@ -225,6 +236,30 @@ class MoeLayer:
             self._h, expert, matrix, bits,
             _ptr(codes, torch.uint8, (rows, cols * bits // 8), "codes"),
             _ptr(scales, torch.float16, (rows, cols // 32), "scales"), _stream(stream)))
+
+    def bind_expert(self, expert: int, tag: int, w=None, q=None, s=None, low_bits=0,
+                    stream=None):
+        """Point an expert at caller-owned device copies: w = [W1, W3, W2] fp16,
+        q / s = codes / scales of the low copy (uint8 / fp16, layout as quantize)."""
+        import torch
+
+        def arr(ts, dtype, name):
+            if ts is None:
+                return None
+            shapes = [(self.f, self.d), (self.f, self.d), (self.d, self.f)]
+            ptrs = []
+            for m, t in enumerate(ts):
+                rows, cols = shapes[m]
+                shp = {torch.float16: (rows, cols)}.get(dtype)
+                if name == "q":
+                    shp = (rows, cols * low_bits // 8)
+                elif name == "s":
+                    shp = (rows, cols // 32)
+                ptrs.append(_ptr(t, dtype, shp, f"{name}[{m}]").value)
+            return (ctypes.c_void_p * 3)(*ptrs)
+        _check(lib().moe_layer_bind_expert(self._h, expert, tag, arr(w, torch.float16, "w"),
+                                           arr(q, torch.uint8, "q"), arr(s, torch.float16, "s"),
+                                           low_bits, _stream(stream)))
 
     def enable_timing(self, on: bool = True):
         _check(lib().moe_layer_enable_timing(self._h, 1 if on else 0))
@@ -372,5 +407,61 @@ class MoeCache:
         try:
             if getattr(self, "_h", None) is not None and self._h.value:
                 lib().moe_cache_destroy(self._h)
+        except Exception:
+            pass
+
+
+class MoeStore:
+    """Pinned host storage of one layer's experts (fp16 + one low copy)."""
+
+    def __init__(self, d_model, d_ff, n_experts, low_bits):
+        self.d, self.f, self.E, self.bits = d_model, d_ff, n_experts, low_bits
+        h = ctypes.c_void_p()
+        _check(lib().moe_store_create(d_model, d_ff, n_experts, low_bits, ctypes.byref(h)))
+        self._h = h
+        a, b, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().moe_store_sizes(h, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
+        self.fp16_bytes, self.code_bytes, self.scale_bytes = a.value, b.value, c.value
+
+    def put(self, expert, w1, w3, w2, stream=None):
+        import torch
+        _check(lib().moe_store_put(
+            self._h, expert, _ptr(w1, torch.float16, (self.f, self.d), "w1"),
+            _ptr(w3, torch.float16, (self.f, self.d), "w3"),
+            _ptr(w2, torch.float16, (self.d, self.f), "w2"), _stream(stream)))
+
+    def slots(self, high, device="cuda"):
+        """Device buffers for one expert copy: ([W1, W3, W2] fp16) or
+        ([codes x3], [scales x3])."""
+        import torch
+        d, f, b = self.d, self.f, self.bits
+        shapes = [(f, d), (f, d), (d, f)]
+        if high:
+            return [torch.empty(s_, dtype=torch.float16, device=device) for s_ in shapes]
+        return ([torch.empty((r, c * b // 8), dtype=torch.uint8, device=device) for r, c in shapes],
+                [torch.empty((r, c // 32), dtype=torch.float16, device=device) for r, c in shapes])
+
+    def load(self, expert, high, dst, stream=None):
+        """dst: [W1, W3, W2] (high) or (codes[3], scales[3]) from slots()."""
+        V3 = ctypes.c_void_p * 3
+        if high:
+            w = V3(*[t.data_ptr() for t in dst])
+            q = s_ = None
+        else:
+            w = None
+            q = V3(*[t.data_ptr() for t in dst[0]])
+            s_ = V3(*[t.data_ptr() for t in dst[1]])
+        _check(lib().moe_store_load(self._h, expert, 1 if high else 0, w, q, s_,
+                                    _stream(stream)))
+
+    def destroy(self):
+        if self._h is not None and self._h.value:
+            _check(lib().moe_store_destroy(self._h))
+        self._h = None
+
+    def __del__(self):
+        try:
+            if getattr(self, "_h", None) is not None and self._h.value:
+                lib().moe_store_destroy(self._h)
         except Exception:
             pass

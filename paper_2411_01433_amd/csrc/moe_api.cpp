@@ -481,6 +481,8 @@ moe_status moe_set_expert_precision(moe_layer_t l, int32_t expert, int32_t tag,
   if (st != MOE_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   ExpertEntry v = l->host_table[expert];
+  if (!v.w[0] || !v.w[1] || !v.w[2])
+    return fail(MOE_ESTATE, "expert %d is bound without fp16 weights: bind it again instead", expert);
   v.tag = tag;
   const int bits = (tag == MOE_TAG_INT4 || tag == MOE_TAG_MISS_INT4) ? 4
                    : (tag == MOE_TAG_INT2 || tag == MOE_TAG_MISS_INT2) ? 2 : 0;
@@ -514,6 +516,42 @@ moe_status moe_set_expert_precision(moe_layer_t l, int32_t expert, int32_t tag,
   }
   l->host_table[expert] = v;
   HIP_TRY(launch_set_entry(l->d_table, expert, v, s), "table update launch");
+  return MOE_OK;
+}
+
+moe_status moe_layer_bind_expert(moe_layer_t l, int32_t expert, int32_t tag,
+                                 const void* const* w, const void* const* q,
+                                 const void* const* sc, int32_t low_bits, void* stream) {
+  g_err.clear();
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  if (expert < 0 || expert >= l->desc.n_experts)
+    return fail(MOE_EINVAL, "expert %d out of range [0, %d)", expert, l->desc.n_experts);
+  if (tag < MOE_TAG_FP16 || tag > MOE_TAG_MISS_INT2) return fail(MOE_EINVAL, "unknown tag %d", tag);
+  const bool need_w = tag == MOE_TAG_FP16 || tag == MOE_TAG_MISS_INT4 || tag == MOE_TAG_MISS_INT2;
+  const int bits = (tag == MOE_TAG_INT4 || tag == MOE_TAG_MISS_INT4) ? 4
+                   : (tag == MOE_TAG_INT2 || tag == MOE_TAG_MISS_INT2) ? 2 : 0;
+  if (bits && low_bits != bits)
+    return fail(MOE_EINVAL, "tag %d needs a %d-bit copy (low_bits %d)", tag, bits, low_bits);
+  for (int m = 0; m < 3; ++m) {
+    if (need_w && (!w || !w[m] || !aligned16(w[m])))
+      return fail(MOE_EINVAL, "tag %d needs three 16-byte aligned fp16 matrices", tag);
+    if (bits && (!q || !sc || !q[m] || !sc[m] || !aligned16(q[m]) || !aligned16(sc[m])))
+      return fail(MOE_EINVAL, "tag %d needs three 16-byte aligned code and scale arrays", tag);
+  }
+  moe_status st = set_device(l);
+  if (st != MOE_OK) return st;
+  ExpertEntry v;
+  std::memset(&v, 0, sizeof v);
+  for (int m = 0; m < 3; ++m) {
+    v.w[m] = need_w ? static_cast<const f16*>(w[m]) : nullptr;
+    v.q[m] = bits ? static_cast<const uint8_t*>(q[m]) : nullptr;
+    v.s[m] = bits ? static_cast<const f16*>(sc[m]) : nullptr;
+  }
+  v.tag = tag;
+  v.low_bits = bits;
+  l->host_table[expert] = v;
+  HIP_TRY(launch_set_entry(l->d_table, expert, v, static_cast<hipStream_t>(stream)),
+          "table update launch");
   return MOE_OK;
 }
 

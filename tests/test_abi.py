@@ -150,3 +150,17 @@ def test_predictor_invalid_handles_fail_cleanly():
     assert L.moe_predict(None, 1, x, x, x, None, x, x, None) == B.MOE_ESTATE
     assert L.moe_predictor_destroy(bogus) == B.MOE_ESTATE
     assert L.moe_predictor_destroy(None) == B.MOE_EINVAL
+
+
+def test_store_and_bind_reject_bad_args():
+    L = B.lib()
+    out = ctypes.c_void_p(123)
+    for args in [(100, 512, 8, 4), (256, 500, 8, 4), (256, 512, 0, 4), (256, 512, 65, 4),
+                 (256, 512, 8, 3), (256, 512, 8, 8)]:
+        assert L.moe_store_create(*args, ctypes.byref(out)) == B.MOE_EINVAL, args
+        assert out.value is None
+    bogus = ctypes.c_void_p(0xdead0)
+    assert L.moe_store_destroy(bogus) == B.MOE_ESTATE
+    assert L.moe_store_destroy(None) == B.MOE_EINVAL
+    assert L.moe_store_sizes(bogus, None, None, None) == B.MOE_ESTATE
+    assert L.moe_layer_bind_expert(bogus, 0, 0, None, None, None, 0, None) == B.MOE_ESTATE
