@@ -483,8 +483,8 @@ def run_cache(args):
 
 
 def run_loading(args):
-    """Dynamic Expert Loader on MI355X (Section 3.1, Section 2.2 "Expert
-    loading dominates"): one Mixtral-shaped expert loaded from pinned host
+    """Dynamic Expert Loader on MI355X (Section 3.2, Fig. 6; Section 2.2:
+    expert loading dominates offloaded inference): one Mixtral-shaped expert loaded from pinned host
     storage into device slots at fp16, int4 and int2 on a copy stream (HIP
     events on that stream), and the 1-token decode step of a resident
     Mixtral-shaped layer timed alone and while loads run beside it."""

@@ -188,10 +188,10 @@ moe_status moe_layer_stage_times(moe_layer_t layer, double* ms,
 moe_status moe_layer_destroy(moe_layer_t layer);
 
 /* ---- Expert storage and loading (Dynamic Expert Loader) ---------------
- * Section 3.1 and Fig. 4: expert copies live in host Expert Storage and a
+ * Section 3.2 and Fig. 6: expert copies live in host Expert Storage and a
  * cache miss loads the copy of the precision the Eq. 2 rule chose into the
- * GPU expert cache; Section 2.2: an int4 copy loads up to 4x faster than
- * the fp16 expert.  A store keeps one layer's experts in pinned host memory
+ * GPU expert cache; Section 2.2: an int4 copy moves about a quarter of the
+ * fp16 bytes, so it loads about four times faster.  A store keeps one layer's experts in pinned host memory
  * (hipHostMalloc): fp16 W1, W3 [d_ff, d_model], W2 [d_model, d_ff] and
  * their low_bits copy (codes + fp16 group scales, the same quantiser and
  * layout as moe_quantize).  Loads are hipMemcpyAsync transfers on the

@@ -1,8 +1,8 @@
 // Expert storage in pinned host memory and the expert loads of the Dynamic
-// Expert Loader (Section 3.1, Fig. 4: expert copies live in host "Expert
-// Storage" and cache misses load the copy of the precision the Eq. 2 rule
-// chose into the GPU expert cache; Section 2.2: an int4 copy loads up to 4x
-// faster than fp16).
+// Expert Loader (Section 3.2, Fig. 6: expert copies live in host Expert
+// Storage and a cache miss loads the copy of the precision the Eq. 2 rule
+// chose into the GPU expert cache; Section 2.2: an int4 copy moves about a
+// quarter of the fp16 bytes, so it loads about four times faster).
 //
 // One store holds one layer's experts: for each, the fp16 W1, W3 [d_ff,
 // d_model] and W2 [d_model, d_ff] and their low-precision copy (codes

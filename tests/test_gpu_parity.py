@@ -236,11 +236,9 @@ def test_token_counts_both_decode_kernels(T):
 
 
 def test_reduction_chunks():
-    """Matrix-core decode with the reduction split into chunks: at 12 tokens
-    the staged activations allow 2048 columns per chunk, so d = 4096 gives
-    two up-projection chunks (partials summed before SwiGLU) and f = 3520
-    two down-projection chunks, the second ragged (1472 columns, a partial
-    last int2 stage); every tag kind."""
+    """Matrix-core decode at 12 tokens over a long reduction: d = 4096 for
+    the up-projection and a ragged f = 3520 for the down-projection (the
+    last int2 stage of a row is partial), every tag kind."""
     wl = _edge("edge_chunks", 37, 4096, 3520, 5, 2, 12,
                [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4, C.TAG_MISS_INT2],
                t1=0.3, t2=0.9)

@@ -1,6 +1,6 @@
 """Expert storage in pinned host memory, asynchronous loads of either
 precision into device slots, and layers bound to those slots (Dynamic
-Expert Loader, Section 3.1 / Fig. 4), through the C ABI.
+Expert Loader, Section 3.2 / Fig. 6), through the C ABI.
 
 Bar: loaded fp16 matrices and low-precision codes and scales are bit-exact
 (equal to the device weights and to the library's own quantised copies);
