@@ -196,14 +196,14 @@ __device__ inline int slot_of(int e) {
   return e < kHalfBlock ? 2 * e : 2 * (e - kHalfBlock) + 1;
 }
 
-// Activation fragments of one stage: lane (t, g) holds columns
+// Activation fragments of one stage, as loaded: lane (t, g) holds columns
 // kk + kLaneCols g + 8j .. +7 of its token row for the steps j.  Chunks past
 // the row end read column 0 instead (their weights are zero).
 template <int BITS> struct AStage {
   f16x8 a[Geo<BITS>::kSteps];
 };
 
-template <int BITS, bool PERM>
+template <int BITS>
 __device__ inline void load_a(const f16* arow, int64_t kk, int64_t ld, AStage<BITS>& a) {
   using GG = Geo<BITS>;
   const int g = (threadIdx.x & 63) >> 4;
@@ -215,26 +215,30 @@ __device__ inline void load_a(const f16* arow, int64_t kk, int64_t ld, AStage<BI
 #pragma unroll
     for (int j = 0; j < kH; ++j)
       a.a[c * kH + j] = *reinterpret_cast<const f16x8*>(arow + col + 8 * j);
-    if (PERM && BITS == 4) {  // x0..x7 -> x0 x4 x1 x5 x2 x6 x3 x7
-#pragma unroll
-      for (int j = 0; j < kH; ++j) {
-        const u32x4 v = __builtin_bit_cast(u32x4, a.a[c * kH + j]);
-        a.a[c * kH + j] = __builtin_bit_cast(
-            f16x8, u32x4{lo_lo(v[0], v[2]), hi_hi(v[0], v[2]), lo_lo(v[1], v[3]), hi_hi(v[1], v[3])});
-      }
-    }
-    if (PERM && BITS == 2) {  // x0..x15 -> x0 x8 x1 x9 .. x3 x11 | x4 x12 .. x7 x15
-#pragma unroll
-      for (int j = 0; j < kH; j += 2) {
-        const u32x4 v0 = __builtin_bit_cast(u32x4, a.a[c * kH + j]);
-        const u32x4 v1 = __builtin_bit_cast(u32x4, a.a[c * kH + j + 1]);
-        a.a[c * kH + j] = __builtin_bit_cast(
-            f16x8, u32x4{lo_lo(v0[0], v1[0]), hi_hi(v0[0], v1[0]), lo_lo(v0[1], v1[1]), hi_hi(v0[1], v1[1])});
-        a.a[c * kH + j + 1] = __builtin_bit_cast(
-            f16x8, u32x4{lo_lo(v0[2], v1[2]), hi_hi(v0[2], v1[2]), lo_lo(v0[3], v1[3]), hi_hi(v0[3], v1[3])});
-      }
-    }
   }
+}
+
+// A fragment of step i in the k-slot order of the dequantised codes (PERM,
+// the up-projection, whose activations are in column order); the
+// down-projection's activations were stored in slot order already.  The
+// permutation is applied at use, not at load: applied at load it would pin
+// a wait for the stage just issued ahead of the scheduling barrier and
+// drain the ring.
+//   int4: x0..x7 -> x0 x4 x1 x5 x2 x6 x3 x7
+//   int2: x0..x15 over steps 2q, 2q+1 -> x0 x8 x1 x9 x2 x10 x3 x11 | x4 x12 .. x7 x15
+template <int BITS, bool PERM>
+__device__ inline f16x8 a_frag(const AStage<BITS>& a, int i) {
+  if (!PERM || BITS == 16) return a.a[i];
+  if (BITS == 4) {
+    const u32x4 v = __builtin_bit_cast(u32x4, a.a[i]);
+    return __builtin_bit_cast(
+        f16x8, u32x4{lo_lo(v[0], v[2]), hi_hi(v[0], v[2]), lo_lo(v[1], v[3]), hi_hi(v[1], v[3])});
+  }
+  const u32x4 v0 = __builtin_bit_cast(u32x4, a.a[i & ~1]);
+  const u32x4 v1 = __builtin_bit_cast(u32x4, a.a[i | 1]);
+  const int o = (i & 1) * 2;
+  return __builtin_bit_cast(f16x8, u32x4{lo_lo(v0[o], v1[o]), hi_hi(v0[o], v1[o]),
+                                         lo_lo(v0[o + 1], v1[o + 1]), hi_hi(v0[o + 1], v1[o + 1])});
 }
 
 // Scales of this lane's chunks for stage kk, zero for chunks past the end:
@@ -261,31 +265,38 @@ __device__ inline void chunk_scales(const WStage<BITS>& w, int64_t kk, int64_t l
   }
 }
 
-// acc[m] += A . W_m over one stage.
+// acc[m] += A . W_m over one stage; each A fragment serves every matrix.
 template <int BITS, int NM>
 __device__ inline void consume(const WStage<BITS> (&w)[NM], const AStage<BITS>& a, int64_t kk,
                                int64_t ld, f32x4 (&acc)[NM]) {
+  constexpr bool kPerm = NM == 2;
+  u32x4 c0[NM], c1[NM];
 #pragma unroll
-  for (int m = 0; m < NM; ++m) {
-    u32x4 c0, c1;
-    exchange<BITS>(w[m], c0, c1);
-    if (BITS == 16) {
-      acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[0], __builtin_bit_cast(f16x8, c0), acc[m], 0, 0, 0);
-      acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[1], __builtin_bit_cast(f16x8, c1), acc[m], 0, 0, 0);
-    } else {
-      f16x2 sc[2][2];
-      chunk_scales<BITS>(w[m], kk, ld, sc);
-      constexpr int kHalf = Geo<BITS>::kSteps / 2;
+  for (int m = 0; m < NM; ++m) exchange<BITS>(w[m], c0[m], c1[m]);
+  if (BITS == 16) {
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
+    for (int m = 0; m < NM; ++m) {
+      acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[0], __builtin_bit_cast(f16x8, c0[m]), acc[m], 0, 0, 0);
+      acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[1], __builtin_bit_cast(f16x8, c1[m]), acc[m], 0, 0, 0);
+    }
+  } else {
+    f16x2 sc[NM][2][2];
 #pragma unroll
-        for (int j = 0; j < kHalf; ++j) {
-          const uint32_t word = c == 0 ? c0[BITS == 4 ? j : j / 2] : c1[BITS == 4 ? j : j / 2];
+    for (int m = 0; m < NM; ++m) chunk_scales<BITS>(w[m], kk, ld, sc[m]);
+    constexpr int kHalf = Geo<BITS>::kSteps / 2;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int j = 0; j < kHalf; ++j) {
+        const f16x8 af = a_frag<BITS, kPerm>(a, c * kHalf + j);
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+          const uint32_t word = c == 0 ? c0[m][BITS == 4 ? j : j / 2] : c1[m][BITS == 4 ? j : j / 2];
           f16x8 b;
-          if (BITS == 4) b = deq4(word, sc[c][0]);
-          else if (j & 1) b = deq2<1>(word, sc[c][j / 4]);
-          else b = deq2<0>(word, sc[c][j / 4]);
-          acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.a[c * kHalf + j], b, acc[m], 0, 0, 0);
+          if (BITS == 4) b = deq4(word, sc[m][c][0]);
+          else if (j & 1) b = deq2<1>(word, sc[m][c][j / 4]);
+          else b = deq2<0>(word, sc[m][c][j / 4]);
+          acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, b, acc[m], 0, 0, 0);
         }
       }
     }
@@ -317,7 +328,7 @@ __device__ inline void tile_gemm(const ExpertEntry& ex, const int (&mats)[NM], i
     const int64_t kk = col(u);
 #pragma unroll
     for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
-    load_a<BITS, NM == 2>(arow, kk, ld, a[u]);
+    load_a<BITS>(arow, kk, ld, a[u]);
   }
   int64_t i0 = 0;
   for (; i0 + D <= nst; i0 += D) {
@@ -327,7 +338,7 @@ __device__ inline void tile_gemm(const ExpertEntry& ex, const int (&mats)[NM], i
       const int64_t kk = col(i0 + u + D);
 #pragma unroll
       for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
-      load_a<BITS, NM == 2>(arow, kk, ld, a[u]);
+      load_a<BITS>(arow, kk, ld, a[u]);
       // keep the ring order: the scheduler would otherwise sink the loads
       // below the products and wait for nearly all of them each round
       __builtin_amdgcn_sched_barrier(0);
