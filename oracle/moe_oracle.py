@@ -20,7 +20,9 @@ What the paper fixes and what is a reading
   - normalisation = softmax over the K selected logits;
   - expert FFN = SwiGLU without bias, W2 (silu(W1 x) * (W3 x));
   - low-precision copy = symmetric signed integer, group of 32 consecutive
-    weights along the input dimension, one fp16 scale per group,
+    weights along the input dimension, one fp16 scale per group (the int8
+    high-precision copy of an int8 model, Section 4.1, is the same
+    quantiser at b = 8),
     s = fp16_rne(max|w| / qmax), q = clamp(rne(w / s), -2^(b-1), qmax),
     qmax = 2^(b-1) - 1; stored offset-binary u = q + 2^(b-1), packed
     little-endian within each byte;
@@ -40,7 +42,7 @@ from dataclasses import dataclass
 import numpy as np
 
 # precision classes of one (token, slot) assignment
-PREC_HIGH = 0   # full-precision (fp16) copy
+PREC_HIGH = 0   # high-precision copy (fp16; int8 for the int8-model tags)
 PREC_LOW = 1    # low-precision copy (int4 or int2, from the expert's tag)
 PREC_SKIP = 2   # expert bypassed (second threshold T2)
 
@@ -50,6 +52,10 @@ TAG_INT4 = 1       # resident as int4 copy: always low (4 bit)
 TAG_INT2 = 2       # resident as int2 copy: always low (2 bit)
 TAG_MISS_INT4 = 3  # cache miss, low copy is int4: Eq. 2 rule decides
 TAG_MISS_INT2 = 4  # cache miss, low copy is int2: Eq. 2 rule decides
+# int8 model (Section 4.1: int2 copies replace int8 experts): the high copy
+# is the expert's int8 quantisation
+TAG_INT8 = 5            # resident as int8 copy: always high (8 bit)
+TAG_MISS_INT8_INT2 = 6  # cache miss, int8 high / int2 low: Eq. 2 rule decides
 
 GROUP = 32
 RMS_EPS = 1e-5
@@ -59,7 +65,14 @@ def low_bits_of_tag(tag: int) -> int:
     """Bit width of the low-precision copy an expert tag refers to (Section 4.1
     Configurations: int4 replaces fp16, int2 replaces int8)."""
     return {TAG_FP16: 0, TAG_INT4: 4, TAG_INT2: 2,
-            TAG_MISS_INT4: 4, TAG_MISS_INT2: 2}[int(tag)]
+            TAG_MISS_INT4: 4, TAG_MISS_INT2: 2,
+            TAG_INT8: 0, TAG_MISS_INT8_INT2: 2}[int(tag)]
+
+
+def high_bits_of_tag(tag: int) -> int:
+    """Bit width of the high-precision copy: 16 (fp16 model) or 8 (int8
+    model, Section 4.1)."""
+    return 8 if int(tag) in (TAG_INT8, TAG_MISS_INT8_INT2) else 16
 
 
 # --------------------------------------------------------------------------
@@ -131,7 +144,7 @@ def token_precisions(w: np.ndarray, sel: np.ndarray, tags: np.ndarray,
     out = np.empty(len(w), dtype=np.int64)
     for j, e in enumerate(sel):
         tag = int(tags[e])
-        if tag == TAG_FP16:
+        if tag in (TAG_FP16, TAG_INT8):
             out[j] = PREC_HIGH
         elif tag in (TAG_INT4, TAG_INT2):
             out[j] = PREC_LOW
@@ -250,7 +263,10 @@ class Expert:
         """float64 weights at the requested precision class (memoised)."""
         memo = self.__dict__.setdefault("_memo", {})
         if prec not in memo:
-            if prec == PREC_HIGH:
+            if prec == PREC_HIGH and high_bits_of_tag(self.tag) == 8:
+                memo[prec] = tuple(make_low_copy(w, 8).dense()
+                                   for w in (self.w1, self.w3, self.w2))
+            elif prec == PREC_HIGH:
                 memo[prec] = (self.w1.astype(np.float64), self.w3.astype(np.float64),
                               self.w2.astype(np.float64))
             else:

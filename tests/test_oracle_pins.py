@@ -157,7 +157,7 @@ def test_quant_worked_examples():
         assert O.unpack_codes(packed, b)[0].tolist() == c["q"]
 
 
-@pytest.mark.parametrize("bits", [4, 2])
+@pytest.mark.parametrize("bits", [4, 2, 8])
 def test_quant_brute_nearest(rng, bits):
     w = _fp16(rng, (6, 64), 0.02)
     w[0, :32] = 0                                   # zero group
@@ -171,7 +171,7 @@ def test_quant_brute_nearest(rng, bits):
             assert q[r, c] == exp, (r, c, float(w[r, c]), float(sf[r, g]))
 
 
-@pytest.mark.parametrize("bits", [4, 2])
+@pytest.mark.parametrize("bits", [4, 2, 8])
 def test_quant_bounds_and_extremes(rng, bits):
     qmax = 2 ** (bits - 1) - 1
     w = _fp16(rng, (64, 256), 0.02)
@@ -196,7 +196,7 @@ def test_quant_bounds_and_extremes(rng, bits):
             assert np.sign(q[r, g * 32 + j]) == np.sign(grp[j])
 
 
-@pytest.mark.parametrize("bits", [4, 2])
+@pytest.mark.parametrize("bits", [4, 2, 8])
 def test_quant_idempotent(rng, bits):
     w = _fp16(rng, (16, 128), 0.02)
     q, s = O.quantize(w, bits)
@@ -220,7 +220,7 @@ def test_quant_subnormal_group():
 
 
 def test_pack_roundtrip_and_layout(rng):
-    for bits in (4, 2):
+    for bits in (4, 2, 8):
         q = rng.integers(-(2 ** (bits - 1)), 2 ** (bits - 1), size=(5, 64))
         p = O.pack_codes(q, bits)
         assert p.shape == (5, 64 * bits // 8) and p.dtype == np.uint8
@@ -300,14 +300,18 @@ def test_layer_k_equals_e_is_soft_moe(rng):
     np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-12)
 
 
-@pytest.mark.parametrize("tag,bits", [(O.TAG_INT4, 4), (O.TAG_INT2, 2)])
-def test_layer_all_low_equals_dense_dequant(rng, tag, bits):
+@pytest.mark.parametrize("tag,bits,prec", [(O.TAG_INT4, 4, O.PREC_LOW), (O.TAG_INT2, 2, O.PREC_LOW),
+                                           (O.TAG_INT8, 8, O.PREC_HIGH)])
+def test_layer_all_quantised_equals_dense_dequant(rng, tag, bits, prec):
+    """Every expert held as one quantised copy (int4 / int2 low copies, or
+    the int8 high copy of an int8 model) equals the dense layer over weights
+    dequantised by the brute-force nearest-level rule."""
     E, d, f, T, K = 4, 64, 96, 4, 2
     x = _fp16(rng, (T, d), 1.0)
     wg = _fp16(rng, (E, d), 0.3)
     ex = _experts(rng, E, d, f, [tag] * E)
     y, r = O.layer_forward(x, wg, ex, K, 1.0, 1.0)
-    assert np.all(r.prec == O.PREC_LOW)
+    assert np.all(r.prec == prec)
 
     def dq(w):  # dequantise by the brute-force nearest-level rule
         w64 = w.astype(np.float64)
@@ -348,6 +352,52 @@ def test_layer_skip_and_mixed(rng):
         lo = [O.make_low_copy(m, 4).dense() for m in (ex[e1].w1, ex[e1].w3, ex[e1].w2)]
         delta = r2.w[t, 1] * O.brute_expert(x[t], *lo)
         np.testing.assert_allclose(y2[t] - y[t], delta, rtol=1e-9, atol=1e-12)
+
+
+def test_layer_int8_model_rule(rng):
+    """int8 model (Section 4.1: int2 copies replace int8 experts) with the
+    thresholds quoted for Mixtral in Section 3.2 (T1 = 0.6, T2 = 0.9).  At
+    top-2 the second slot's Eq. 2 score is the first gate w0, so it runs from
+    the int8 copy when w0 <= 0.6, from the int2 copy when 0.6 < w0 <= 0.9 and
+    is skipped above; the first slot always runs from the int8 copy.  Each
+    token's output is rebuilt by brute force from nearest-level codes."""
+    E, d, f, T, K = 4, 32, 64, 24, 2
+    x = _fp16(rng, (T, d), 1.0)
+    wg = _fp16(rng, (E, d), 0.6)
+    tags = [O.TAG_INT8, O.TAG_MISS_INT8_INT2, O.TAG_MISS_INT8_INT2, O.TAG_INT8]
+    ex = _experts(rng, E, d, f, tags)
+    y, r = O.layer_forward(x, wg, ex, K, 0.6, 0.9)
+
+    def dq(w, bits):
+        w64 = w.astype(np.float64)
+        qmax = 2 ** (bits - 1) - 1
+        out = np.zeros_like(w64)
+        for rr in range(w.shape[0]):
+            for g in range(w.shape[1] // 32):
+                seg = w64[rr, g * 32:(g + 1) * 32]
+                s = float(np.float16(np.abs(seg).max() / qmax))
+                out[rr, g * 32:(g + 1) * 32] = [O.brute_nearest_code(v, s, bits) * s for v in seg]
+        return out
+    seen = set()
+    for t in range(T):
+        ref = np.zeros(d)
+        for j in range(K):
+            e = int(r.idx[t, j])
+            if j == 0 or tags[e] == O.TAG_INT8:
+                exp_p = O.PREC_HIGH
+            else:
+                w0 = r.w[t, 0]
+                exp_p = O.PREC_HIGH if w0 <= 0.6 else (O.PREC_LOW if w0 <= 0.9 else O.PREC_SKIP)
+            assert r.prec[t, j] == exp_p
+            if tags[e] == O.TAG_MISS_INT8_INT2 and j == 1:
+                seen.add(exp_p)
+            if exp_p == O.PREC_SKIP:
+                continue
+            bits = 8 if exp_p == O.PREC_HIGH else 2
+            mats = [dq(m, bits) for m in (ex[e].w1, ex[e].w3, ex[e].w2)]
+            ref += r.w[t, j] * O.brute_expert(x[t], *mats)
+        np.testing.assert_allclose(y[t], ref, rtol=1e-10, atol=1e-12)
+    assert seen == {O.PREC_HIGH, O.PREC_LOW, O.PREC_SKIP}, seen
 
 
 def test_layer_linear_in_expert_output(rng):
