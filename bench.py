@@ -93,6 +93,15 @@ def expert_bytes(d, f, bits):
     return 2 * matrix_bytes(f, d, bits) + matrix_bytes(d, f, bits)
 
 
+def copy_bits(tag, prec):
+    """Bit width of the copy a (tag, precision class) pair streams: the high
+    copy is fp16, or int8 for the int8-model tags (5, 6); the low copy is
+    int4 for tags 1 and 3, else int2."""
+    if prec == 0:
+        return 8 if tag in (5, 6) else 16
+    return 4 if tag in (1, 3) else 2
+
+
 def step_bytes(wl, idx, prec, tags):
     """Algorithmic bytes of one step: every distinct (expert, precision) copy
     the step streams, plus the gate; and the up-projection's share."""
@@ -101,7 +110,7 @@ def step_bytes(wl, idx, prec, tags):
     for e, p in zip(idx.ravel(), prec.ravel()):
         if p == 2:
             continue
-        bits = 16 if p == 0 else (4 if tags[int(e)] in (1, 3) else 2)
+        bits = copy_bits(int(tags[int(e)]), int(p))
         copies.add((int(e), bits))
     T, K = idx.shape
     n_pairs = int((prec != 2).sum())

@@ -70,7 +70,12 @@ typedef enum {
     MOE_TAG_INT4 = 1,       /* resident as its int4 copy: always int4 */
     MOE_TAG_INT2 = 2,       /* resident as its int2 copy: always int2 */
     MOE_TAG_MISS_INT4 = 3,  /* cache miss, low copy int4: Eq. 2 rule decides */
-    MOE_TAG_MISS_INT2 = 4   /* cache miss, low copy int2: Eq. 2 rule decides */
+    MOE_TAG_MISS_INT2 = 4,  /* cache miss, low copy int2: Eq. 2 rule decides */
+    /* int8 models (Section 4.1: int2 copies replace int8 experts): the high
+     * copy is the expert's int8 quantisation (same quantiser, b = 8) */
+    MOE_TAG_INT8 = 5,           /* resident as its int8 copy: always int8 */
+    MOE_TAG_MISS_INT8_INT2 = 6  /* cache miss, int8 high / int2 low copy:
+                                   Eq. 2 rule decides */
 } moe_tag;
 
 /* Precision class used for one (token, slot), as reported in prec_used. */
@@ -113,10 +118,11 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
                           moe_layer_t* out);
 
 /* Set an expert's precision tag (Section 3.2 / 3.4: its cache state).  A tag
- * that needs a low-precision copy builds it from the fp16 weights with the
- * quantiser above the first time (allocating it: library-owned, freed by
- * moe_layer_destroy); the table entry is updated in stream order, so calls
- * enqueued later on `stream` see the new tag. */
+ * that needs a quantised copy (int4 / int2 low copies; the int8 high copy of
+ * MOE_TAG_INT8 and MOE_TAG_MISS_INT8_INT2) builds it from the fp16 weights
+ * with the quantiser below the first time (allocating it: library-owned,
+ * freed by moe_layer_destroy); the table entry is updated in stream order,
+ * so calls enqueued later on `stream` see the new tag. */
 moe_status moe_set_expert_precision(moe_layer_t layer, int32_t expert,
                                     int32_t tag, void* stream);
 
@@ -154,8 +160,8 @@ moe_status moe_prefill_residual(moe_layer_t layer, int32_t n_tokens,
                                 int32_t* topk_idx, float* topk_w,
                                 int8_t* prec_used, void* stream);
 
-/* Copy an expert's low-precision copy out (for inspection and parity).
- *  matrix  0 = W1, 1 = W3, 2 = W2;  bits 4 or 2 (the copy must exist)
+/* Copy an expert's quantised copy out (for inspection and parity).
+ *  matrix  0 = W1, 1 = W3, 2 = W2;  bits 8, 4 or 2 (the copy must exist)
  *  codes   device u8 [rows, cols*bits/8];  scales device fp16 [rows, cols/32]
  * where [rows, cols] is the matrix's shape. */
 moe_status moe_export_packed(moe_layer_t layer, int32_t expert, int32_t matrix,
@@ -165,7 +171,7 @@ moe_status moe_export_packed(moe_layer_t layer, int32_t expert, int32_t matrix,
 /* Quantise any fp16 matrix with the layer's quantiser (the format above).
  *  w       device fp16 [rows, cols]; cols a multiple of 32
  *  codes   device u8 [rows, cols*bits/8];  scales device fp16 [rows, cols/32]
- *  bits    4 or 2.  Needs no handle. */
+ *  bits    8, 4 or 2.  Needs no handle. */
 moe_status moe_quantize(const void* w, int64_t rows, int64_t cols, int32_t bits,
                         void* codes, void* scales, void* stream);
 
@@ -230,7 +236,8 @@ moe_status moe_store_destroy(moe_store_t store);
  * they must outlive their use), in stream order on `stream`: tag FP16
  * needs w[3] (fp16, layout as moe_layer_init); INT4 / INT2 need q[3], s[3]
  * with low_bits 4 / 2 (layout as moe_quantize); MISS_INT4 / MISS_INT2 need
- * all of them.  Pointers must be 16-byte aligned.  An expert bound without
+ * all of them.  The int8-model tags (INT8, MISS_INT8_INT2) are not bindable
+ * (MOE_EUNSUPPORTED).  Pointers must be 16-byte aligned.  An expert bound without
  * fp16 weights cannot take moe_set_expert_precision (MOE_ESTATE) until it
  * is bound again; moe_export_packed reports only library-built copies. */
 moe_status moe_layer_bind_expert(moe_layer_t layer, int32_t expert, int32_t tag,
@@ -348,9 +355,11 @@ moe_status moe_cache_replay(moe_cache_t cache, int64_t n, const int32_t* tokens,
                             const int32_t* layers, const int32_t* experts, const int32_t* highs,
                             const uint8_t* new_sequence, int32_t* hits, int32_t* evicted);
 
-/* Tags of the n_experts experts of one layer (host int32 array): FP16 when
- * the high copy is resident, else MISS_INT4 / MISS_INT2 (bits_lo 4 / 2;
- * other widths: MOE_EUNSUPPORTED) so that the Eq. 2 rule decides per token. */
+/* Tags of the n_experts experts of one layer (host int32 array) so that the
+ * Eq. 2 rule decides per token for the missing ones: bits 16/4 and 16/2
+ * give FP16 when the high copy is resident, else MISS_INT4 / MISS_INT2;
+ * bits 8/2 (an int8 model) give INT8, else MISS_INT8_INT2; other widths
+ * MOE_EUNSUPPORTED. */
 moe_status moe_cache_layer_tags(moe_cache_t cache, int32_t layer, int32_t* tags);
 
 /* Accumulated miss penalty and counts since creation (NULL outputs skipped). */

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libmoe.so")
 
 MOE_OK, MOE_EINVAL, MOE_ENOMEM, MOE_EHIP, MOE_ESTATE, MOE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 TAG_FP16, TAG_INT4, TAG_INT2, TAG_MISS_INT4, TAG_MISS_INT2 = 0, 1, 2, 3, 4
+TAG_INT8, TAG_MISS_INT8_INT2 = 5, 6  # int8 models: int8 high copy, int2 low copy
 PREC_HIGH, PREC_LOW, PREC_SKIP = 0, 1, 2
 
 EXPORTED = (

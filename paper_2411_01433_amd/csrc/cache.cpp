@@ -275,11 +275,15 @@ moe_status moe_cache_layer_tags(moe_cache_t c, int32_t layer, int32_t* tags) {
   moe_status st = check_ix(c, layer, 0);
   if (st != MOE_OK) return st;
   if (!tags) return cfail(MOE_EINVAL, "tags is NULL");
-  if (c->d.bits_lo != 4 && c->d.bits_lo != 2)
-    return cfail(MOE_EUNSUPPORTED, "layer tags need a 4- or 2-bit low-precision copy");
-  const int32_t miss = c->d.bits_lo == 4 ? MOE_TAG_MISS_INT4 : MOE_TAG_MISS_INT2;
+  // fp16 models pair with int4 or int2 copies, int8 models with int2
+  // (Section 4.1)
+  const int hi = c->d.bits_hi, lo = c->d.bits_lo;
+  if (!((hi == 16 && (lo == 4 || lo == 2)) || (hi == 8 && lo == 2)))
+    return cfail(MOE_EUNSUPPORTED, "layer tags need bits 16/4, 16/2 or 8/2 (got %d/%d)", hi, lo);
+  const int32_t hit = hi == 8 ? MOE_TAG_INT8 : MOE_TAG_FP16;
+  const int32_t miss = hi == 8 ? MOE_TAG_MISS_INT8_INT2 : lo == 4 ? MOE_TAG_MISS_INT4 : MOE_TAG_MISS_INT2;
   for (int32_t e = 0; e < c->d.n_experts; ++e)
-    tags[e] = c->in_hi[layer * c->d.n_experts + e] ? MOE_TAG_FP16 : miss;
+    tags[e] = c->in_hi[layer * c->d.n_experts + e] ? hit : miss;
   return MOE_OK;
 }
 

@@ -1,6 +1,6 @@
 // Decode-path expert kernels: fused dequantise-GEMV for the SwiGLU experts
-// of Eq. 1 at fp16, int4 or int2, with the weighted combine fused into the
-// down-projection.
+// of Eq. 1 at fp16, int8 (the high copy of an int8 model), int4 or int2,
+// with the weighted combine fused into the down-projection.
 //
 //   up:    h[p, r] = silu(W1[r,:] . x_t) * (W3[r,:] . x_t)        (fp16 out)
 //   down:  y[t, r] = sum over the (token, slot) pairs p of token t of
@@ -13,6 +13,7 @@
 // the up-projection).
 // Per lane and chunk a wave reads one piece per row:
 //   fp16  16 bytes =  8 weights   (chunk =  512 columns)
+//   int8  16 bytes = 16 weights   (chunk = 1024 columns, half a group)
 //   int4   8 bytes = 16 weights   (chunk = 1024 columns, half a group)
 //   int2   4 bytes = 16 weights   (chunk = 1024 columns, half a group)
 // so each wave-wide load covers 1 KiB, 512 B or 256 B of one row.  Codes are
@@ -35,7 +36,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kMaxChunkTokens = 8;  // tokens per register tile
 
 // Output rows per block for a token tile of up to NTMAX tokens.  Small
 // tiles measured fastest at one or two tokens: more blocks in flight hide
@@ -78,12 +78,14 @@ __device__ inline const __attribute__((address_space(1))) T* gmem(const T* p) {
 // Elements per lane per chunk for each weight format.
 template <int BITS> struct Fmt;
 template <> struct Fmt<16> { static constexpr int kEpl = 8; };
+template <> struct Fmt<8> { static constexpr int kEpl = 16; };
 template <> struct Fmt<4> { static constexpr int kEpl = 16; };
 template <> struct Fmt<2> { static constexpr int kEpl = 16; };
 
 // Activations of one lane for one chunk, as the dword pairs the weight
-// pieces are dotted with.  fp16: natural order (4 dwords).  int4: per 8
-// elements (x0,x4)(x1,x5)(x2,x6)(x3,x7) (8 dwords).  int2: per 16 elements
+// pieces are dotted with.  fp16: natural order (4 dwords).  int8: per 4
+// elements (x0,x2)(x1,x3) (8 dwords).  int4: per 8 elements
+// (x0,x4)(x1,x5)(x2,x6)(x3,x7) (8 dwords).  int2: per 16 elements
 // (x0,x8)(x1,x9)...(x7,x15) (8 dwords).
 template <int BITS>
 __device__ inline void load_act(const f16* p, uint32_t (&a)[Fmt<BITS>::kEpl / 2]) {
@@ -93,7 +95,12 @@ __device__ inline void load_act(const f16* p, uint32_t (&a)[Fmt<BITS>::kEpl / 2]
   } else {
     const u32x4 v0 = reinterpret_cast<const u32x4*>(p)[0];
     const u32x4 v1 = reinterpret_cast<const u32x4*>(p)[1];
-    if constexpr (BITS == 4) {  // blocks of 8: dwords (x0x1)(x2x3)(x4x5)(x6x7)
+    if constexpr (BITS == 8) {  // blocks of 4: dwords (x0x1)(x2x3)
+      a[0] = lo_lo(v0.x, v0.y); a[1] = hi_hi(v0.x, v0.y);
+      a[2] = lo_lo(v0.z, v0.w); a[3] = hi_hi(v0.z, v0.w);
+      a[4] = lo_lo(v1.x, v1.y); a[5] = hi_hi(v1.x, v1.y);
+      a[6] = lo_lo(v1.z, v1.w); a[7] = hi_hi(v1.z, v1.w);
+    } else if constexpr (BITS == 4) {  // blocks of 8: dwords (x0x1)(x2x3)(x4x5)(x6x7)
       a[0] = lo_lo(v0.x, v0.z); a[1] = hi_hi(v0.x, v0.z);
       a[2] = lo_lo(v0.y, v0.w); a[3] = hi_hi(v0.y, v0.w);
       a[4] = lo_lo(v1.x, v1.z); a[5] = hi_hi(v1.x, v1.z);
@@ -123,6 +130,30 @@ template <> struct Piece<16> {
     acc = dot2(v.y, a[1], acc);
     acc = dot2(v.z, a[2], acc);
     return dot2(v.w, a[3], acc);
+  }
+};
+
+template <> struct Piece<8> {
+  u32x4 v;
+  f16 s;
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, int64_t ld, int64_t col) {
+    v = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.hq[m] + row * ld + col)));
+    s = __builtin_nontemporal_load(gmem(ex.hs[m] + row * (ld / kGroup) + col / kGroup));
+  }
+  // word holding e0..e3 (e_j in byte j) -> pairs (e0, e2), (e1, e3) - 128
+  static __device__ inline float dot_word(uint32_t w, const uint32_t* a, float g) {
+    const f16x2 bias = as_h2(0x64806480u);  // 1152 = 1024 + 128
+    const f16x2 q0 = as_h2((w & 0x00FF00FFu) | 0x64006400u) - bias;
+    const f16x2 q1 = as_h2(((w >> 8) & 0x00FF00FFu) | 0x64006400u) - bias;
+    g = dot2(__builtin_bit_cast(uint32_t, q0), a[0], g);
+    return dot2(__builtin_bit_cast(uint32_t, q1), a[1], g);
+  }
+  __device__ inline float dot(const uint32_t (&a)[8], float acc) const {
+    float g = dot_word(v.x, a, 0.0f);
+    g = dot_word(v.y, a + 2, g);
+    g = dot_word(v.z, a + 4, g);
+    g = dot_word(v.w, a + 6, g);
+    return fmaf((float)s, g, acc);
   }
 };
 
@@ -282,6 +313,7 @@ __global__ __launch_bounds__(kThreads) void decode_up_kernel(
   const int64_t row0 = (int64_t)blockIdx.x * UpRows<NTMAX>::value;
   const int32_t* pairs = perm + g.offset;
   if (g.bits == 16) up_group<16, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, red);
+  else if (g.bits == 8) up_group<8, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, red);
   else if (g.bits == 4) up_group<4, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, red);
   else up_group<2, NTMAX>(ex, pairs, g.count, x, h, d, f, K, row0, red);
 }
@@ -347,6 +379,7 @@ __global__ __launch_bounds__(kThreads) void decode_down_kernel(
     const ExpertEntry ex = table[g.expert];
     const int32_t* pairs = perm + g.offset;
     if (g.bits == 16) down_group<16, NTMAX>(ex, pairs, g.count, h, gate_w, f, K, row0, red, yacc);
+    else if (g.bits == 8) down_group<8, NTMAX>(ex, pairs, g.count, h, gate_w, f, K, row0, red, yacc);
     else if (g.bits == 4) down_group<4, NTMAX>(ex, pairs, g.count, h, gate_w, f, K, row0, red, yacc);
     else down_group<2, NTMAX>(ex, pairs, g.count, h, gate_w, f, K, row0, red, yacc);
   }
@@ -379,24 +412,19 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
     x_next[base + c] = (f16)(h_res[base + c] * r);
 }
 
-int nt_max(int T) {
-  const int n = T < kMaxChunkTokens ? T : kMaxChunkTokens;
-  return n <= 1 ? 1 : (n <= 2 ? 2 : (n <= 4 ? 4 : 8));
-}
+// The host takes these kernels for one or two tokens per step; from three
+// tokens the matrix-core kernels run instead.
+int nt_max(int T) { return T <= 1 ? 1 : 2; }
 
 }  // namespace
 
 hipError_t launch_decode_up(const ExpertEntry* table, const WorkList* wl,
                             const int32_t* perm, const f16* x, f16* h, int T,
                             int d, int f, int K, int max_groups, hipStream_t s) {
-  const int nt = nt_max(T);
-  dim3 grid(f / (nt <= 2 ? UpRows<1>::value : UpRows<8>::value), max_groups);
-  switch (nt) {
-    case 1: decode_up_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
-    case 2: decode_up_kernel<2><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
-    case 4: decode_up_kernel<4><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
-    default: decode_up_kernel<8><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K); break;
-  }
+  if (T < 1 || T > 2) return hipErrorInvalidValue;
+  dim3 grid(f / UpRows<2>::value, max_groups);
+  if (nt_max(T) == 1) decode_up_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K);
+  else decode_up_kernel<2><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K);
   return hipGetLastError();
 }
 
@@ -404,14 +432,12 @@ hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
                               const int32_t* perm, const float* gate_w,
                               const f16* h, float* y, float* h_res, int T, int d,
                               int f, int K, hipStream_t s) {
-  const int nt = nt_max(T);
-  dim3 grid(d / (nt <= 2 ? DownRows<1>::value : DownRows<8>::value));
-  switch (nt) {
-    case 1: decode_down_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
-    case 2: decode_down_kernel<2><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
-    case 4: decode_down_kernel<4><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
-    default: decode_down_kernel<8><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K); break;
-  }
+  if (T < 1 || T > 2) return hipErrorInvalidValue;
+  dim3 grid(d / DownRows<2>::value);
+  if (nt_max(T) == 1)
+    decode_down_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K);
+  else
+    decode_down_kernel<2><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K);
   return hipGetLastError();
 }
 

@@ -13,8 +13,8 @@
 // MFMA lane layout: A[l%16][8(l/16)+i], B[8(l/16)+i][l%16], C[4(l/16)+i][l%16].
 //
 // Weight streaming.  A block owns 16 rows of one or two matrices; its waves
-// take turns along the reduction dimension in stages of 128 bytes per row (64 fp16 columns, 256
-// int4 or 512 int2 codes).  Each of the two 16-byte loads of a stage covers
+// take turns along the reduction dimension in stages of 128 bytes per row
+// (64 fp16 columns, 128 int8, 256 int4 or 512 int2 codes).  Each of the two 16-byte loads of a stage covers
 // 8 rows x one full 128-byte line: lane l reads chunk l/8 of row
 // 8i + l%8 (i = 0, 1).  A DPP row rotation by 8 with bank masks then moves
 // the chunks so that lane (n = l%16, g = l/16) holds chunks 2g and 2g+1 of
@@ -51,7 +51,7 @@ template <int BITS> struct Geo {
   static constexpr int kChunkCols = kCols / 8;   // columns of one 16-byte chunk
   static constexpr int kSteps = kCols / 32;      // MFMA k-steps
   static constexpr int kScales = BITS == 16 ? 0 : kLaneCols / kGroup;  // per lane
-  static constexpr int kDepth = BITS == 16 ? 4 : (BITS == 4 ? 2 : 1);
+  static constexpr int kDepth = BITS == 16 ? 4 : BITS == 8 ? 3 : BITS == 4 ? 2 : 1;
 };
 
 // DPP: lane i of each 16-lane row reads lane i^8 (rotation by 8); BANKS
@@ -82,21 +82,23 @@ template <int BITS>
 __device__ inline WSrc<BITS> wsrc(const ExpertEntry& ex, int m, int64_t row0, int64_t ld) {
   const int l = threadIdx.x & 63;
   const int64_t rb = ld * BITS / 8;
-  const uint8_t* base = BITS == 16 ? reinterpret_cast<const uint8_t*>(ex.w[m]) : ex.q[m];
+  const uint8_t* base = BITS == 16 ? reinterpret_cast<const uint8_t*>(ex.w[m])
+                        : BITS == 8 ? ex.hq[m] : ex.q[m];
   WSrc<BITS> s;
   s.chunk = l >> 3;
   s.row = base + (row0 + (l & 7)) * rb + 16 * s.chunk;
   s.row8 = 8 * rb;
   s.ngr = (int)(ld / kGroup);
   s.srow = BITS == 16 ? nullptr
-                      : ex.s[m] + (row0 + (l & 15)) * s.ngr + Geo<BITS>::kScales * (l >> 4);
+                      : (BITS == 8 ? ex.hs[m] : ex.s[m]) + (row0 + (l & 15)) * s.ngr +
+                            Geo<BITS>::kScales * (l >> 4);
   return s;
 }
 
 // Load stage kk (first column, a multiple of the stage width).  Chunks past
 // the row end (the last stage of a code row may be partial) read the row's
-// first chunk instead and get scale 0 at use; scales are read in group
-// pairs clamped to the row.  Nothing outside the row is touched.
+// first chunk instead and get scale 0 at use; scales are read in aligned
+// group pairs clamped to the row.  Nothing outside the row is touched.
 template <int BITS>
 __device__ inline void load_w(const WSrc<BITS>& s, int64_t kk, int64_t ld, WStage<BITS>& w) {
   using G = const __attribute__((address_space(1))) u32x4*;
@@ -114,7 +116,8 @@ __device__ inline void load_w(const WSrc<BITS>& s, int64_t kk, int64_t ld, WStag
     const int gi = (int)(kk / kGroup) + Geo<BITS>::kScales * g;  // first group of the lane
 #pragma unroll
     for (int h = 0; h < (BITS == 2 ? 2 : 1); ++h) {
-      const int idx = min(gi + 2 * h, s.ngr - 2);
+      // int8: one group per lane, read with its even neighbour
+      const int idx = min(BITS == 8 ? (gi & ~1) : gi + 2 * h, s.ngr - 2);
       w.s[h] = __builtin_nontemporal_load(
           reinterpret_cast<S>(gmem(s.srow - Geo<BITS>::kScales * g + idx)));
     }
@@ -178,6 +181,20 @@ __device__ inline f16x8 deq2(uint32_t w, f16x2 s2) {
   }
 }
 
+// int8: codes e0..e7 in the bytes of (w0, w1).  A byte swap first puts e0,
+// e1 (and e2, e3) 16 bits apart, so the and-or pairs come out in column
+// order: (e0,e1)(e2,e3)(e4,e5)(e6,e7), no activation permutation needed.
+__device__ inline uint32_t swap_mid_bytes(uint32_t w) {  // b0 b1 b2 b3 -> b0 b2 b1 b3
+  return __builtin_amdgcn_perm(w, w, 0x03010200u);
+}
+__device__ inline f16x8 deq8(uint32_t w0, uint32_t w1, f16x2 s2) {
+  const uint32_t a = swap_mid_bytes(w0), b = swap_mid_bytes(w1);
+  return pack8(scaled(pair_bits(a, 0x00FF00FFu, 0x64006400u), 0x64806480u, s2),        // 1024 + 128
+               scaled(pair_bits(a >> 8, 0x00FF00FFu, 0x64006400u), 0x64806480u, s2),
+               scaled(pair_bits(b, 0x00FF00FFu, 0x64006400u), 0x64806480u, s2),
+               scaled(pair_bits(b >> 8, 0x00FF00FFu, 0x64006400u), 0x64806480u, s2));
+}
+
 // low halves of (a, b) / high halves of (a, b) as one dword
 __device__ inline uint32_t lo_lo(uint32_t a, uint32_t b) {
   return __builtin_amdgcn_perm(b, a, 0x05040100u);
@@ -228,7 +245,7 @@ __device__ inline void load_a(const f16* arow, int64_t kk, int64_t ld, AStage<BI
 //   int2: x0..x15 over steps 2q, 2q+1 -> x0 x8 x1 x9 x2 x10 x3 x11 | x4 x12 .. x7 x15
 template <int BITS, bool PERM>
 __device__ inline f16x8 a_frag(const AStage<BITS>& a, int i) {
-  if (!PERM || BITS == 16) return a.a[i];
+  if (!PERM || BITS == 16 || BITS == 8) return a.a[i];
   if (BITS == 4) {
     const u32x4 v = __builtin_bit_cast(u32x4, a.a[i]);
     return __builtin_bit_cast(
@@ -253,10 +270,12 @@ __device__ inline void chunk_scales(const WStage<BITS>& w, int64_t kk, int64_t l
     const bool ok = kk + GG::kLaneCols * g + GG::kChunkCols * (c + 1) <= ld;
     // integer splats: a vector-element read of the packed pair went through
     // scratch memory
-    const uint32_t sp = BITS == 4 ? w.s[0] : w.s[c];
+    const uint32_t sp = BITS == 2 ? w.s[c] : w.s[0];
     const uint32_t lo = __builtin_amdgcn_perm(sp, sp, 0x01000100u);
     const uint32_t hi = __builtin_amdgcn_perm(sp, sp, 0x03020302u);
-    if (BITS == 4) {  // one group per chunk: halves of s[0]
+    if (BITS == 8) {  // one group per lane group: the half of s[0] its parity picks
+      sc[c][0] = sc[c][1] = as_h2(ok ? (((kk / kGroup + g) & 1) ? hi : lo) : 0u);
+    } else if (BITS == 4) {  // one group per chunk: halves of s[0]
       sc[c][0] = sc[c][1] = as_h2(ok ? (c == 1 ? hi : lo) : 0u);
     } else {          // two groups per chunk: s[c]
       sc[c][0] = as_h2(ok ? lo : 0u);
@@ -291,9 +310,11 @@ __device__ inline void consume(const WStage<BITS> (&w)[NM], const AStage<BITS>& 
         const f16x8 af = a_frag<BITS, kPerm>(a, c * kHalf + j);
 #pragma unroll
         for (int m = 0; m < NM; ++m) {
-          const uint32_t word = c == 0 ? c0[m][BITS == 4 ? j : j / 2] : c1[m][BITS == 4 ? j : j / 2];
+          const u32x4& cw = c == 0 ? c0[m] : c1[m];
+          const uint32_t word = cw[BITS == 8 ? 2 * j : BITS == 4 ? j : j / 2];
           f16x8 b;
-          if (BITS == 4) b = deq4(word, sc[m][c][0]);
+          if (BITS == 8) b = deq8(word, cw[2 * j + 1], sc[m][c][0]);
+          else if (BITS == 4) b = deq4(word, sc[m][c][0]);
           else if (j & 1) b = deq2<1>(word, sc[m][c][j / 4]);
           else b = deq2<0>(word, sc[m][c][j / 4]);
           acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af, b, acc[m], 0, 0, 0);
@@ -394,7 +415,7 @@ __device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* p
           const float a = acc[0][i], b = acc[1][i];
           // low-precision groups store h in the down-projection's slot order
           constexpr int kBlk = BITS == 4 ? 8 : 16;
-          const int64_t hc = BITS == 16 ? row
+          const int64_t hc = BITS >= 8 ? row
                              : (row & ~(int64_t)(kBlk - 1)) + slot_of<BITS>((int)(row & (kBlk - 1)));
           h[(int64_t)pairs[tok] * f + hc] = (f16)(a / (1.0f + expf(-a)) * b);
         }
@@ -413,6 +434,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void decode_up_mfma_kernel(
   const ExpertEntry ex = table[g.expert];
   const int64_t row0 = (int64_t)blockIdx.x * 16;
   if (g.bits == 16) up_group<16>(ex, g, perm, x, h, d, f, K, row0, red);
+  else if (g.bits == 8) up_group<8>(ex, g, perm, x, h, d, f, K, row0, red);
   else if (g.bits == 4) up_group<4>(ex, g, perm, x, h, d, f, K, row0, red);
   else up_group<2>(ex, g, perm, x, h, d, f, K, row0, red);
 }
@@ -452,6 +474,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void decode_down_mfma_kernel(
   const ExpertEntry ex = table[g.expert];
   const int64_t row0 = (int64_t)blockIdx.x * 16;
   if (g.bits == 16) down_group<16>(ex, g, perm, h, e, d, f, row0, red);
+  else if (g.bits == 8) down_group<8>(ex, g, perm, h, e, d, f, row0, red);
   else if (g.bits == 4) down_group<4>(ex, g, perm, h, e, d, f, row0, red);
   else down_group<2>(ex, g, perm, h, e, d, f, row0, red);
 }

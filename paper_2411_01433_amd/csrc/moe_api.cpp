@@ -44,6 +44,21 @@ moe_status hip_fail(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Copy slot of a quantised bit width: 4, 2 (low copies), 8 (int8 high copy).
+int slot_of_bits(int bits) { return bits == 4 ? 0 : bits == 2 ? 1 : 2; }
+
+// Bit widths a tag's copies need: the low copy (4, 2 or 0) and the high
+// copy (16: the borrowed fp16 weights, 8: an int8 copy, 0: none).
+int low_bits_of(int tag) {
+  return (tag == MOE_TAG_INT4 || tag == MOE_TAG_MISS_INT4) ? 4
+         : (tag == MOE_TAG_INT2 || tag == MOE_TAG_MISS_INT2 || tag == MOE_TAG_MISS_INT8_INT2) ? 2
+                                                                                             : 0;
+}
+int high_bits_of(int tag) {
+  if (tag == MOE_TAG_INT8 || tag == MOE_TAG_MISS_INT8_INT2) return 8;
+  return (tag == MOE_TAG_FP16 || tag == MOE_TAG_MISS_INT4 || tag == MOE_TAG_MISS_INT2) ? 16 : 0;
+}
+
 }  // namespace
 
 struct moe_layer {
@@ -51,10 +66,10 @@ struct moe_layer {
   int device = -1;
   const f16* w_router = nullptr;
   std::vector<ExpertEntry> host_table;
-  // library-owned low-precision copies: [expert][bits==4 ? 0 : 1][matrix]
+  // library-owned quantised copies: [expert][slot_of_bits(bits)][matrix]
   std::vector<void*> owned;
-  std::vector<std::array<std::array<uint8_t*, 3>, 2>> low_q;
-  std::vector<std::array<std::array<f16*, 3>, 2>> low_s;
+  std::vector<std::array<std::array<uint8_t*, 3>, 3>> low_q;
+  std::vector<std::array<std::array<f16*, 3>, 3>> low_s;
   // device memory
   ExpertEntry* d_table = nullptr;
   WorkList* d_wl = nullptr;
@@ -423,6 +438,7 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
     x.w[1] = static_cast<const f16*>(w3[e]);
     x.w[2] = static_cast<const f16*>(w2[e]);
     x.tag = TAG_FP16;
+    x.hi_bits = 16;
     for (auto& a : l->low_q[e]) a.fill(nullptr);
     for (auto& a : l->low_s[e]) a.fill(nullptr);
   }
@@ -476,7 +492,7 @@ moe_status moe_set_expert_precision(moe_layer_t l, int32_t expert, int32_t tag,
   if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
   if (expert < 0 || expert >= l->desc.n_experts)
     return fail(MOE_EINVAL, "expert %d out of range [0, %d)", expert, l->desc.n_experts);
-  if (tag < MOE_TAG_FP16 || tag > MOE_TAG_MISS_INT2) return fail(MOE_EINVAL, "unknown tag %d", tag);
+  if (tag < MOE_TAG_FP16 || tag > MOE_TAG_MISS_INT8_INT2) return fail(MOE_EINVAL, "unknown tag %d", tag);
   moe_status st = set_device(l);
   if (st != MOE_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -484,11 +500,10 @@ moe_status moe_set_expert_precision(moe_layer_t l, int32_t expert, int32_t tag,
   if (!v.w[0] || !v.w[1] || !v.w[2])
     return fail(MOE_ESTATE, "expert %d is bound without fp16 weights: bind it again instead", expert);
   v.tag = tag;
-  const int bits = (tag == MOE_TAG_INT4 || tag == MOE_TAG_MISS_INT4) ? 4
-                   : (tag == MOE_TAG_INT2 || tag == MOE_TAG_MISS_INT2) ? 2 : 0;
-  if (bits) {
-    const int slot = bits == 4 ? 0 : 1;
-    const int d = l->desc.d_model, f = l->desc.d_ff;
+  // quantised copies this tag needs, built once from the fp16 weights
+  const int d = l->desc.d_model, f = l->desc.d_ff;
+  auto ensure = [&](int bits, const uint8_t* (&q_out)[3], const f16* (&s_out)[3]) -> moe_status {
+    const int slot = slot_of_bits(bits);
     for (int m = 0; m < 3; ++m) {
       const int64_t rows = m < 2 ? f : d, cols = m < 2 ? d : f;
       if (!l->low_q[expert][slot][m]) {
@@ -506,14 +521,23 @@ moe_status moe_set_expert_precision(moe_layer_t l, int32_t expert, int32_t tag,
         HIP_TRY(launch_quantize(v.w[m], rows, cols, bits, static_cast<uint8_t*>(q),
                                 static_cast<f16*>(sc), s), "quantize kernel launch");
       }
-      v.q[m] = l->low_q[expert][slot][m];
-      v.s[m] = l->low_s[expert][slot][m];
+      q_out[m] = l->low_q[expert][slot][m];
+      s_out[m] = l->low_s[expert][slot][m];
     }
-    v.low_bits = bits;
-  } else {
-    for (int m = 0; m < 3; ++m) { v.q[m] = nullptr; v.s[m] = nullptr; }
-    v.low_bits = 0;
+    return MOE_OK;
+  };
+  const int lb = low_bits_of(tag), hb = high_bits_of(tag);
+  for (int m = 0; m < 3; ++m) { v.q[m] = nullptr; v.s[m] = nullptr; v.hq[m] = nullptr; v.hs[m] = nullptr; }
+  if (lb) {
+    st = ensure(lb, v.q, v.s);
+    if (st != MOE_OK) return st;
   }
+  if (hb == 8) {
+    st = ensure(8, v.hq, v.hs);
+    if (st != MOE_OK) return st;
+  }
+  v.low_bits = lb;
+  v.hi_bits = hb == 8 ? 8 : 16;
   l->host_table[expert] = v;
   HIP_TRY(launch_set_entry(l->d_table, expert, v, s), "table update launch");
   return MOE_OK;
@@ -526,6 +550,8 @@ moe_status moe_layer_bind_expert(moe_layer_t l, int32_t expert, int32_t tag,
   if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
   if (expert < 0 || expert >= l->desc.n_experts)
     return fail(MOE_EINVAL, "expert %d out of range [0, %d)", expert, l->desc.n_experts);
+  if (tag == MOE_TAG_INT8 || tag == MOE_TAG_MISS_INT8_INT2)
+    return fail(MOE_EUNSUPPORTED, "int8-model tags are set with moe_set_expert_precision, not bound");
   if (tag < MOE_TAG_FP16 || tag > MOE_TAG_MISS_INT2) return fail(MOE_EINVAL, "unknown tag %d", tag);
   const bool need_w = tag == MOE_TAG_FP16 || tag == MOE_TAG_MISS_INT4 || tag == MOE_TAG_MISS_INT2;
   const int bits = (tag == MOE_TAG_INT4 || tag == MOE_TAG_MISS_INT4) ? 4
@@ -549,6 +575,7 @@ moe_status moe_layer_bind_expert(moe_layer_t l, int32_t expert, int32_t tag,
   }
   v.tag = tag;
   v.low_bits = bits;
+  v.hi_bits = 16;
   l->host_table[expert] = v;
   HIP_TRY(launch_set_entry(l->d_table, expert, v, static_cast<hipStream_t>(stream)),
           "table update launch");
@@ -588,9 +615,9 @@ moe_status moe_export_packed(moe_layer_t l, int32_t expert, int32_t matrix, int3
   if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
   if (expert < 0 || expert >= l->desc.n_experts) return fail(MOE_EINVAL, "expert out of range");
   if (matrix < 0 || matrix > 2) return fail(MOE_EINVAL, "matrix must be 0, 1 or 2");
-  if (bits != 4 && bits != 2) return fail(MOE_EINVAL, "bits must be 4 or 2");
+  if (bits != 8 && bits != 4 && bits != 2) return fail(MOE_EINVAL, "bits must be 8, 4 or 2");
   if (!codes || !scales) return fail(MOE_EINVAL, "codes and scales must not be NULL");
-  const int slot = bits == 4 ? 0 : 1;
+  const int slot = slot_of_bits(bits);
   const uint8_t* q = l->low_q[expert][slot][matrix];
   const f16* sc = l->low_s[expert][slot][matrix];
   if (!q) return fail(MOE_ESTATE, "expert %d has no int%d copy", expert, bits);
@@ -611,11 +638,12 @@ moe_status moe_quantize(const void* w, int64_t rows, int64_t cols, int32_t bits,
   g_err.clear();
   if (!w || !codes || !scales) return fail(MOE_EINVAL, "pointers must not be NULL");
   if (rows < 0 || cols < 0 || cols % kGroup) return fail(MOE_EINVAL, "cols must be a multiple of 32");
-  if (bits != 4 && bits != 2) return fail(MOE_EINVAL, "bits must be 4 or 2");
+  if (bits != 8 && bits != 4 && bits != 2) return fail(MOE_EINVAL, "bits must be 8, 4 or 2");
   if (rows > 0 && cols / kGroup > (((int64_t)1 << 38) / rows)) return fail(MOE_EINVAL, "matrix too large");
   if (!aligned16(w) || ((uintptr_t)codes & 7u) || ((uintptr_t)scales & 1u))
     return fail(MOE_EINVAL, "w must be 16-byte aligned, codes 8-byte, scales 2-byte");
-  if (bits == 4 && ((uintptr_t)codes & 15u)) return fail(MOE_EINVAL, "int4 codes must be 16-byte aligned");
+  if (bits >= 4 && ((uintptr_t)codes & 15u))
+    return fail(MOE_EINVAL, "int4 and int8 codes must be 16-byte aligned");
   HIP_TRY(launch_quantize(static_cast<const f16*>(w), rows, cols, bits,
                           static_cast<uint8_t*>(codes), static_cast<f16*>(scales),
                           static_cast<hipStream_t>(stream)), "quantize kernel launch");

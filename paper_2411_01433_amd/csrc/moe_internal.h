@@ -24,7 +24,7 @@ constexpr int kDecodeMaxTokens = 64;
 
 enum { PREC_HIGH = 0, PREC_LOW = 1, PREC_SKIP = 2 };
 enum { TAG_FP16 = 0, TAG_INT4 = 1, TAG_INT2 = 2, TAG_MISS_INT4 = 3,
-       TAG_MISS_INT2 = 4 };
+       TAG_MISS_INT2 = 4, TAG_INT8 = 5, TAG_MISS_INT8_INT2 = 6 };
 
 // Device-side expert table entry: where each copy of one expert lives and
 // which cache state (tag) it is in.
@@ -32,16 +32,19 @@ struct ExpertEntry {
   const f16* w[3];       // fp16 W1, W3 ([f, d]) and W2 ([d, f]); borrowed
   const uint8_t* q[3];   // packed codes of the low copy (bits = low_bits)
   const f16* s[3];       // fp16 group scales of the low copy
+  const uint8_t* hq[3];  // int8 codes of the high copy when hi_bits == 8
+  const f16* hs[3];      // fp16 group scales of the int8 high copy
   int32_t tag;           // TAG_*
   int32_t low_bits;      // 4 or 2 when a low copy exists, else 0
-  int32_t pad[2];
+  int32_t hi_bits;       // 16 (fp16 high copy) or 8 (int8 high copy)
+  int32_t pad;
 };
 
 // One work group: every (token, slot) pair routed to `expert` at one
 // precision.  Pairs are listed contiguously in perm[offset, offset+count).
 struct Group {
   int32_t expert;
-  int32_t bits;    // 16 (fp16 copy), 4 or 2
+  int32_t bits;    // 16 (fp16 copy), 8 (int8 high copy), 4 or 2
   int32_t offset;
   int32_t count;
 };

@@ -1,5 +1,6 @@
 // Prefill path: the experts of Eq. 1 as an MFMA grouped GEMM with the
-// low-precision copies dequantised in registers, then the weighted combine.
+// quantised copies (int4 / int2 low copies, the int8 high copy of an int8
+// model) dequantised in registers, then the weighted combine.
 //
 //   up:    H[j, r] = silu(X_g W1^T)[j, r] * (X_g W3^T)[j, r]     (fp16 out)
 //   down:  E[j, r] = (H_g W2^T)[j, r]                             (fp32 out)
@@ -24,6 +25,8 @@
 // into registers during the MFMAs) and weight fragments are loaded two
 // stages ahead, straight into registers:
 //   fp16: lane group g (= l/16) reads 16 B at k = 32s + 8g for step s;
+//   int8: lane group g reads the 16 B of columns 16g..16g+15 of the stage
+//         and step s uses its words 2s, 2s+1;
 //   int4: lane group g reads the 8 B half group of columns 16g..16g+15 of
 //         the stage and step s uses its word s;
 //   int2: lane group g reads the 4 B of the same columns, half-word s.
@@ -119,6 +122,10 @@ struct ActStager {
   }
 };
 
+// int4 / int2 groups stage their activations permuted (perm8); fp16 and
+// int8 groups in column order.
+template <int BITS> constexpr bool kPermuted = BITS == 4 || BITS == 2;
+
 // A fragment (activations) of token tile tt for step s of the stage.
 template <int BITS>
 __device__ inline f16x8 a_frag(const f16* lds, int tt, int s) {
@@ -144,6 +151,38 @@ template <> struct WFrag<16> {
     }
   }
   __device__ inline f16x8 get(int s) const { return __builtin_bit_cast(f16x8, v[s]); }
+};
+
+template <> struct WFrag<8> {
+  u32x4 q;
+  f16 sc;
+  // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
+  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
+                              int64_t ld, int64_t k0) {
+    const int g = (threadIdx.x & 63) >> 4;
+    const int64_t col = k0 + 16 * g;
+    if (ok && col < ld) {
+      q = *gmem(reinterpret_cast<const u32x4*>(ex.hq[m] + row * ld + col));
+      sc = *gmem(ex.hs[m] + row * (ld / kGroup) + col / kGroup);
+    } else {
+      q = u32x4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};  // q = 0
+      sc = (f16)0.0f;
+    }
+  }
+  // bytes e0..e3 of a word, middle bytes swapped (e0 e2 e1 e3), pair as
+  // (e0,e1)(e2,e3) in column order, scaled
+  __device__ inline f16x8 get(int s) const {
+    const f16x2 bias = as_h2(0x64806480u);  // 1152 = 1024 + 128
+    const f16x2 s2 = {sc, sc};
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const uint32_t w = __builtin_amdgcn_perm(q[2 * s + k], q[2 * s + k], 0x03010200u);
+      o[2 * k] = as_u32((as_h2((w & 0x00FF00FFu) | 0x64006400u) - bias) * s2);
+      o[2 * k + 1] = as_u32((as_h2(((w >> 8) & 0x00FF00FFu) | 0x64006400u) - bias) * s2);
+    }
+    return pack8(o[0], o[1], o[2], o[3]);
+  }
 };
 
 template <> struct WFrag<4> {
@@ -246,7 +285,7 @@ __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
       f16* cur = lds + buf * (kPassTok * kLdsRow);
       // the buffer written here was last read two stages ago, before the
       // previous stage's barrier
-      st.store<0, BITS != 16>(cur);
+      st.store<0, kPermuted<BITS>>(cur);
       __syncthreads();
       if (k0 + kStageK < ld) st.fetch<0>(act_ld, k0 + kStageK);
       WFrag<BITS> w2[RT][NM];
@@ -288,8 +327,8 @@ __device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
       f16* cur = lds + u * (kPassTok * kLdsRow);
       // the buffer written here was last read two stages ago, before the
       // previous stage's barrier; its activations were fetched two stages ago
-      if (u == 0) st.store<0, BITS != 16>(cur);
-      else st.store<1, BITS != 16>(cur);
+      if (u == 0) st.store<0, kPermuted<BITS>>(cur);
+      else st.store<1, kPermuted<BITS>>(cur);
       __syncthreads();
       if (u == 0) st.fetch<0>(act_ld, k0 + 2 * kStageK);
       else st.fetch<1>(act_ld, k0 + 2 * kStageK);
@@ -373,6 +412,7 @@ __global__ __launch_bounds__(kThreads) void prefill_up_kernel(
   const Group g = wl->groups[gi];
   const ExpertEntry ex = table[g.expert];
   if (g.bits == 16) up_group<16>(ex, g, perm, x, h, d, f, K, tile, lds);
+  else if (g.bits == 8) up_group<8>(ex, g, perm, x, h, d, f, K, tile, lds);
   else if (g.bits == 4) up_group<4>(ex, g, perm, x, h, d, f, K, tile, lds);
   else up_group<2>(ex, g, perm, x, h, d, f, K, tile, lds);
 }
@@ -411,6 +451,7 @@ __global__ __launch_bounds__(kThreads) void prefill_down_kernel(
   const Group g = wl->groups[gi];
   const ExpertEntry ex = table[g.expert];
   if (g.bits == 16) down_group<16>(ex, g, h, e, d, f, tile, lds);
+  else if (g.bits == 8) down_group<8>(ex, g, h, e, d, f, tile, lds);
   else if (g.bits == 4) down_group<4>(ex, g, h, e, d, f, tile, lds);
   else down_group<2>(ex, g, h, e, d, f, tile, lds);
 }

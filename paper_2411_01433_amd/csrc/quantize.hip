@@ -1,21 +1,24 @@
-// Group-wise symmetric quantiser producing the low-precision expert copies
+// Group-wise symmetric quantiser producing the quantised expert copies
 // (Section 2.2 and Section 4.1 "Configurations": int4 replaces fp16, int2
-// replaces int8).  Format: group of 32 consecutive weights along a row,
+// replaces int8; the int8 copy itself is the high precision of an int8
+// model).  Format: group of 32 consecutive weights along a row,
 // s = fp16_rne(max|w| / qmax), q = clamp(rne(w / s), -2^(b-1), qmax),
 // stored offset-binary and packed little-endian within each byte.
 //
-// Exactness: w and s are fp16, so w / s is never within 2^-12 of a
-// half-integer unless it is one; one correctly rounded fp32 division then
-// makes the same rounding decision as exact arithmetic.  max|w| / 7 has a
-// period-3 binary expansion (or is exact), so rounding it to fp32 and then
-// to fp16 cannot land on an fp16 midpoint: the double rounding equals a
-// single rounding.  Divisions therefore use __fdiv_rn, never a reciprocal.
+// Exactness: w and s are fp16, so w / s is never within 2^-13 of a
+// half-integer unless it is one, while one correctly rounded fp32 division
+// of a quotient below 128 errs by at most 2^-17: it makes the same rounding
+// decision as exact arithmetic.  max|w| / 7 and max|w| / 127 have binary
+// expansions of period 3 and 7 (or are exact), so rounding them to fp32 and
+// then to fp16 cannot land on an fp16 midpoint (that needs a run of 12 equal
+// bits): the double rounding equals a single rounding.  Divisions therefore
+// use __fdiv_rn, never a reciprocal.
 #include "moe_internal.h"
 
 namespace moe {
 
-// One thread per group of 32 weights: 64 contiguous input bytes, 16 (int4)
-// or 8 (int2) output bytes and one fp16 scale.
+// One thread per group of 32 weights: 64 contiguous input bytes, 32 (int8),
+// 16 (int4) or 8 (int2) output bytes and one fp16 scale.
 template <int BITS>
 __global__ __launch_bounds__(256) void quantize_kernel(
     const f16* __restrict__ w, int64_t n_groups, uint8_t* __restrict__ codes,
@@ -56,7 +59,10 @@ __global__ __launch_bounds__(256) void quantize_kernel(
     const int bit = j * BITS;
     out[bit >> 5] |= u << (bit & 31);
   }
-  if (BITS == 4) {
+  if (BITS == 8) {
+    reinterpret_cast<u32x4*>(codes)[2 * g] = u32x4{out[0], out[1], out[2], out[3]};
+    reinterpret_cast<u32x4*>(codes)[2 * g + 1] = u32x4{out[4], out[5], out[6], out[7]};
+  } else if (BITS == 4) {
     reinterpret_cast<u32x4*>(codes)[g] = u32x4{out[0], out[1], out[2], out[3]};
   } else {
     reinterpret_cast<uint2*>(codes)[g] = make_uint2(out[0], out[1]);
@@ -70,7 +76,10 @@ hipError_t launch_quantize(const f16* w, int64_t rows, int64_t cols, int bits,
   if (n_groups == 0) return hipSuccess;
   const int threads = 256;
   const int64_t blocks = (n_groups + threads - 1) / threads;
-  if (bits == 4)
+  if (bits == 8)
+    quantize_kernel<8><<<dim3((unsigned)blocks), dim3(threads), 0, s>>>(
+        w, n_groups, codes, scales);
+  else if (bits == 4)
     quantize_kernel<4><<<dim3((unsigned)blocks), dim3(threads), 0, s>>>(
         w, n_groups, codes, scales);
   else

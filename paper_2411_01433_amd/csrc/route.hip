@@ -121,7 +121,7 @@ __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
     const int e = sel[k];
     const int tag = tags[e];
     int prec;
-    if (tag == TAG_FP16) {
+    if (tag == TAG_FP16 || tag == TAG_INT8) {
       prec = PREC_HIGH;
     } else if (tag == TAG_INT4 || tag == TAG_INT2) {
       prec = PREC_LOW;
@@ -147,13 +147,18 @@ __device__ void decide_token(const RouteParams& p, int t, const float* lrow,
 
 // Stable counting sort of all T*K pairs by key = expert*2 + (low ? 1 : 0)
 // (skipped pairs get no key).  Run by one whole block of kRouteThreads.
+// Copy widths of one expert packed in one int: low copy (4, 2 or 0) in
+// bits 0-7, high copy (16 or 8) in bits 8-15.
+__device__ inline int pack_widths(const ExpertEntry& x) { return x.low_bits | (x.hi_bits << 8); }
+__device__ inline int copy_bits(int widths, int low) { return low ? (widths & 0xFF) : (widths >> 8); }
+
 // Pairs are taken one block-wide chunk at a time; inside a wave, lanes with
 // equal keys are found with one ballot per distinct key, and a lane's rank
 // among them is the number of lower lanes in that ballot; per-wave counts
 // are then scanned across waves, so pair order inside a group is the pair
 // index order.
 __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
-                               const int8_t* prec, const int* low_bits,
+                               const int8_t* prec, const int* widths,
                                WorkList* wl, int32_t* perm, int32_t* pos) {
   constexpr int kW = kRouteThreads / 64;
   __shared__ int cnt[kMaxKeys];
@@ -179,7 +184,7 @@ __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
         const int e = k >> 1;
         Group g;
         g.expert = e;
-        g.bits = (k & 1) ? low_bits[e] : 16;
+        g.bits = copy_bits(widths[e], k & 1);
         g.offset = off;
         g.count = c;
         wl->groups[ng++] = g;
@@ -228,11 +233,11 @@ __device__ void build_worklist(const RouteParams& p, const int32_t* idx,
   }
 }
 
-// Expert tags and low-copy widths into LDS.
-__device__ inline void stage_table(const RouteParams& p, int* tags, int* low_bits) {
+// Expert tags and copy widths into LDS.
+__device__ inline void stage_table(const RouteParams& p, int* tags, int* widths) {
   for (int e = threadIdx.x; e < p.E; e += blockDim.x) {
     tags[e] = p.table[e].tag;
-    low_bits[e] = p.table[e].low_bits;
+    widths[e] = pack_widths(p.table[e]);
   }
 }
 
@@ -240,16 +245,16 @@ __device__ inline void stage_table(const RouteParams& p, int* tags, int* low_bit
 // the LDS stores after them, so the two memory round trips overlap (E is at
 // most 64, below the block size).
 struct TableRow {
-  int tag, low_bits;
+  int tag, widths;
   __device__ inline void load(const RouteParams& p) {
     const int e = threadIdx.x;
     tag = e < p.E ? p.table[e].tag : 0;
-    low_bits = e < p.E ? p.table[e].low_bits : 0;
+    widths = e < p.E ? pack_widths(p.table[e]) : 0;
   }
-  __device__ inline void store(const RouteParams& p, int* tags, int* lb) const {
+  __device__ inline void store(const RouteParams& p, int* tags, int* wd) const {
     if ((int)threadIdx.x < p.E) {
       tags[threadIdx.x] = tag;
-      lb[threadIdx.x] = low_bits;
+      wd[threadIdx.x] = widths;
     }
   }
 };
@@ -362,7 +367,7 @@ __device__ void decide_wave(const RouteParams& p, const float* lg, const int* ta
       const int e = sel[k];
       const int tag = tags[e];
       int prec;
-      if (tag == TAG_FP16) {
+      if (tag == TAG_FP16 || tag == TAG_INT8) {
         prec = PREC_HIGH;
       } else if (tag == TAG_INT4 || tag == TAG_INT2) {
         prec = PREC_LOW;
@@ -390,7 +395,7 @@ __device__ void decide_wave(const RouteParams& p, const float* lg, const int* ta
 // wave: keys in increasing order, one ballot each; a pair's rank is the
 // number of lower lanes with the same key.
 __device__ void worklist_wave(const RouteParams& p, const int32_t* idx, const int8_t* prec,
-                              const int* low_bits, WorkList* wl, int32_t* perm, int32_t* pos) {
+                              const int* widths, WorkList* wl, int32_t* perm, int32_t* pos) {
   const int lane = threadIdx.x & 63;
   const int N = p.T * p.K;
   int key = -1;
@@ -413,7 +418,7 @@ __device__ void worklist_wave(const RouteParams& p, const int32_t* idx, const in
     if (lane == 0) {
       Group g;
       g.expert = k >> 1;
-      g.bits = (k & 1) ? low_bits[k >> 1] : 16;
+      g.bits = copy_bits(widths[k >> 1], k & 1);
       g.offset = off;
       g.count = c;
       wl->groups[ng] = g;
@@ -432,7 +437,7 @@ __device__ void worklist_wave(const RouteParams& p, const int32_t* idx, const in
 __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
     RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
   __shared__ float lg[kDecodeMaxTokens * kMaxExperts];
-  __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
+  __shared__ int tags[kMaxExperts], widths[kMaxExperts];
   __shared__ int32_t s_idx[kDecodeMaxTokens * kMaxTopK];
   __shared__ int8_t s_prec[kDecodeMaxTokens * kMaxTopK];
   __shared__ __attribute__((aligned(16))) f16 xs[kFastXBytes / 2];
@@ -443,14 +448,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
   else if (p.T == 1) gate_logits<1, 8>(p, 0, p.T, lg);
   else if (p.T == 2) gate_logits<2, 8>(p, 0, p.T, lg);
   else gate_logits<4, 4>(p, 0, p.T, lg);
-  tr.store(p, tags, low_bits);
+  tr.store(p, tags, widths);
   __syncthreads();
   decide_wave(p, lg, tags, o, s_idx, s_prec);
   __syncthreads();
   if (p.T * p.K <= 64) {
-    if (threadIdx.x < 64) worklist_wave(p, s_idx, s_prec, low_bits, wl, perm, pos);
+    if (threadIdx.x < 64) worklist_wave(p, s_idx, s_prec, widths, wl, perm, pos);
   } else {
-    build_worklist(p, s_idx, s_prec, low_bits, wl, perm, pos);
+    build_worklist(p, s_idx, s_prec, widths, wl, perm, pos);
   }
 }
 
@@ -458,10 +463,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
 __global__ __launch_bounds__(kPrefillThreads) void route_tokens_kernel(
     RouteParams p, RouteOut o) {
   __shared__ float lg[kPrefillTokPerBlock * kMaxExperts];
-  __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
+  __shared__ int tags[kMaxExperts], widths[kMaxExperts];
   const int t0 = blockIdx.x * kPrefillTokPerBlock;
   const int t1 = min(t0 + kPrefillTokPerBlock, p.T);
-  stage_table(p, tags, low_bits);
+  stage_table(p, tags, widths);
   gate_logits<kPrefillTokPerBlock, 8>(p, t0, t1, lg);
   __syncthreads();
   for (int t = t0 + (int)threadIdx.x; t < t1; t += blockDim.x)
@@ -470,10 +475,10 @@ __global__ __launch_bounds__(kPrefillThreads) void route_tokens_kernel(
 
 __global__ __launch_bounds__(kRouteThreads) void worklist_kernel(
     RouteParams p, RouteOut o, WorkList* wl, int32_t* perm, int32_t* pos) {
-  __shared__ int tags[kMaxExperts], low_bits[kMaxExperts];
-  stage_table(p, tags, low_bits);
+  __shared__ int tags[kMaxExperts], widths[kMaxExperts];
+  stage_table(p, tags, widths);
   __syncthreads();
-  build_worklist(p, o.idx, o.prec, low_bits, wl, perm, pos);
+  build_worklist(p, o.idx, o.prec, widths, wl, perm, pos);
 }
 
 }  // namespace

@@ -1,4 +1,4 @@
-"""The five synthetic workloads: shapes, seeds, tags and input recipes.
+"""The synthetic workloads: shapes, seeds, tags and input recipes.
 
 Shapes come from the paper's model table (Mixtral-8x7B: d_model 4096,
 d_ff 14336, 8 experts, top-2; Phi-MoE: d_model 4096, d_ff 6400, 16 experts,
@@ -19,6 +19,7 @@ from .gen import (TENSOR_TAGS, TENSOR_W1, TENSOR_W2, TENSOR_W3, TENSOR_WG,
 
 # tag values (mirrors the library's enum; plain data, no method arithmetic)
 TAG_FP16, TAG_INT4, TAG_INT2, TAG_MISS_INT4, TAG_MISS_INT2 = 0, 1, 2, 3, 4
+TAG_INT8, TAG_MISS_INT8_INT2 = 5, 6
 
 W_STD = 0.02
 X_STD = 1.0
@@ -80,7 +81,16 @@ MIXTRAL_PREFILL = Workload(
     mode="prefill", residual=True, tag_recipe="431",
     note="per-layer seeded 4:3:1 map; MFMA grouped GEMM")
 
-ALL = [TINY, MIXTRAL_T1, MIXTRAL_T8_SKEW, PHI_STACK, MIXTRAL_PREFILL]
+# int8 model (Section 4.1: int2 copies replace int8 experts), thresholds as
+# quoted for Mixtral in Section 3.2: every Eq. 2 outcome (int8, int2, skip)
+MIXTRAL_INT8_T1 = Workload(
+    name="mixtral_int8_layer_decode_t1", seed=5, d_model=4096, d_ff=14336,
+    n_experts=8, top_k=2, n_tokens=1, t1=0.6, t2=0.9,
+    fixed_tags=(TAG_INT8,) * 4 + (TAG_MISS_INT8_INT2,) * 4,
+    note="int8 model: experts 0-3 cached int8; 4-7 miss -> int8 / int2 / skip "
+         "(Eq. 2 with T1 = 0.6, T2 = 0.9)")
+
+ALL = [TINY, MIXTRAL_T1, MIXTRAL_T8_SKEW, PHI_STACK, MIXTRAL_PREFILL, MIXTRAL_INT8_T1]
 BY_NAME = {w.name: w for w in ALL}
 
 

@@ -108,14 +108,21 @@ def test_layer_tags():
     c.access(1, 2, True)
     c.access(1, 3, False)
     assert c.layer_tags(1).tolist() == [B.TAG_MISS_INT4] * 2 + [B.TAG_FP16, B.TAG_MISS_INT4]
+    # an int8 model (Section 4.1): int8 high copies, int2 low copies
     c2 = P.MoeCache(1, 2, 1, 1, 1.0, 0.0, 0.0, 0.0, bits_hi=8, bits_lo=2)
     c2.begin_token()
     c2.access(0, 1, True)
-    assert c2.layer_tags(0).tolist() == [B.TAG_MISS_INT2, B.TAG_FP16]
-    c3 = P.MoeCache(1, 2, 1, 1, 1.0, 0.0, 0.0, 0.0, bits_hi=8, bits_lo=3)
-    with pytest.raises(B.MoeError):
-        c3.layer_tags(0)
-    for h in (c, c2, c3):
+    assert c2.layer_tags(0).tolist() == [B.TAG_MISS_INT8_INT2, B.TAG_INT8]
+    c4 = P.MoeCache(1, 2, 1, 1, 1.0, 0.0, 0.0, 0.0, bits_hi=16, bits_lo=2)
+    c4.begin_token()
+    c4.access(0, 0, True)
+    assert c4.layer_tags(0).tolist() == [B.TAG_FP16, B.TAG_MISS_INT2]
+    for hi, lo in ((8, 3), (8, 4), (12, 2)):
+        c3 = P.MoeCache(1, 2, 1, 1, 1.0, 0.0, 0.0, 0.0, bits_hi=hi, bits_lo=lo)
+        with pytest.raises(B.MoeError):
+            c3.layer_tags(0)
+        c3.destroy()
+    for h in (c, c2, c4):
         h.destroy()
 
 

@@ -108,7 +108,7 @@ def _quant_cases():
     return cases
 
 
-@pytest.mark.parametrize("bits", [4, 2])
+@pytest.mark.parametrize("bits", [8, 4, 2])
 def test_quantize_bit_exact(bits):
     for w in _quant_cases():
         if w.shape[1] % 32:
