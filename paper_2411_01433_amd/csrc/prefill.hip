@@ -15,12 +15,12 @@
 //
 // Tiling (v_mfma_f32_16x16x32_f16: lane l holds A[l%16][8(l/16)+i],
 // B[8(l/16)+i][l%16] and C[4(l/16)+i][l%16]): M = tokens (A = activations
-// from LDS, up to 192 per pass = 12 tiles), N = weight rows (B = weight
+// from LDS, up to 160 per pass = 10 tiles), N = weight rows (B = weight
 // rows, each lane's 8 k-values contiguous in memory), K = reduction dim in
-// stages of 64.  A block of 8 waves owns 8 x 16 weight rows; each wave owns
-// 16 rows for all the pass's tokens (up to 192), so every weight element is
+// stages of 64.  A block of 4 waves owns 4 x 16 weight rows; each wave owns
+// 16 rows for all the pass's tokens (up to 160), so every weight element is
 // fetched from HBM once per pass and used by every token of the group, and
-// each staged activation tile serves 128 weight rows.  Activations are
+// each staged activation tile serves 64 weight rows.  Activations are
 // double-buffered in LDS (one barrier per stage, the next stage fetched
 // into registers during the MFMAs) and weight fragments are loaded two
 // stages ahead, straight into registers:
@@ -43,11 +43,14 @@ namespace moe {
 
 namespace {
 
-constexpr int kThreads = 512;
-constexpr int kWaves = 8;
+// 4 waves per block, two blocks per compute unit: a stage barrier holds
+// only its block's waves, and the other block runs meanwhile (up-projection
+// 528 -> 484 us per Mixtral-shaped 512-token layer against 8-wave blocks).
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
 constexpr int kStageK = 64;               // reduction columns per stage (2 MFMA steps)
 constexpr int kSteps = kStageK / 32;
-constexpr int kPassTok = 192;             // tokens per pass (12 MFMA tiles)
+constexpr int kPassTok = 160;             // tokens per pass (10 MFMA tiles)
 constexpr int kTokTiles = kPassTok / 16;
 constexpr int kLdsRow = kStageK + 8;      // halves per staged row (16 B pad)
 constexpr int kUpRowsW = 16;              // weight rows per wave, up-projection
@@ -402,7 +405,7 @@ __device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* p
 // XCD whatever the group's precision) and the tiles of one group, which
 // read the same activation columns at about the same time, share them in
 // each XCD's L2.
-__global__ __launch_bounds__(kThreads) void prefill_up_kernel(
+__global__ __launch_bounds__(kThreads, 2) void prefill_up_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
     const int32_t* __restrict__ perm, const f16* __restrict__ x, f16* __restrict__ h,
     int d, int f, int K, int n_tiles) {
@@ -442,7 +445,7 @@ __device__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
   }
 }
 
-__global__ __launch_bounds__(kThreads) void prefill_down_kernel(
+__global__ __launch_bounds__(kThreads, 2) void prefill_down_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
     const f16* __restrict__ h, float* __restrict__ e, int d, int f, int n_tiles) {
   __shared__ f16 lds[2 * kPassTok * kLdsRow];
