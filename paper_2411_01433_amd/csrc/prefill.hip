@@ -465,15 +465,17 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
+constexpr int kCombineThreads = 512;
+
 // y[t] = sum_k w[t,k] * E[pos(t,k)] in slot order (skip -> 0); with h_res:
 // h_res[t] += that and x_next[t] = fp16(rmsnorm(h_res[t])).  One block per
 // token, 4 columns per thread per step (d is a multiple of 64).
-__global__ __launch_bounds__(kThreads) void combine_prefill_kernel(
+__global__ __launch_bounds__(kCombineThreads) void combine_prefill_kernel(
     const float* __restrict__ e, const int32_t* __restrict__ pos,
     const float* __restrict__ w, const int8_t* __restrict__ prec, int d, int K,
     float* __restrict__ y, float* __restrict__ h_res, f16* __restrict__ x_next,
     float eps) {
-  __shared__ float red[kWaves];
+  __shared__ float red[kCombineThreads / 64];
   __shared__ int s_pos[kMaxTopK];
   __shared__ float s_w[kMaxTopK];
   const int t = blockIdx.x;
@@ -485,7 +487,7 @@ __global__ __launch_bounds__(kThreads) void combine_prefill_kernel(
   __syncthreads();
   const int64_t base = (int64_t)t * d;
   float ss = 0.0f;
-  for (int c = threadIdx.x * 4; c < d; c += kThreads * 4) {
+  for (int c = threadIdx.x * 4; c < d; c += kCombineThreads * 4) {
     f32x4 acc = {0, 0, 0, 0};
     for (int k = 0; k < K; ++k)
       if (s_pos[k] >= 0) {
@@ -506,9 +508,9 @@ __global__ __launch_bounds__(kThreads) void combine_prefill_kernel(
   __syncthreads();
   float tot = 0.0f;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) tot += red[i];
+  for (int i = 0; i < kCombineThreads / 64; ++i) tot += red[i];
   const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x * 4; c < d; c += kThreads * 4) {
+  for (int c = threadIdx.x * 4; c < d; c += kCombineThreads * 4) {
     const f32x4 hv = *reinterpret_cast<const f32x4*>(h_res + base + c);
     f16x4 o;
     o[0] = (f16)(hv.x * r); o[1] = (f16)(hv.y * r); o[2] = (f16)(hv.z * r); o[3] = (f16)(hv.w * r);
@@ -542,7 +544,7 @@ hipError_t launch_prefill_down(const ExpertEntry* table, const WorkList* wl,
 hipError_t launch_combine_prefill(const float* e, const int32_t* pos, const float* w,
                                   const int8_t* prec, int T, int d, int K, float* y,
                                   float* h_res, f16* x_next, float eps, hipStream_t s) {
-  combine_prefill_kernel<<<T, kThreads, 0, s>>>(e, pos, w, prec, d, K, y, h_res, x_next, eps);
+  combine_prefill_kernel<<<T, kCombineThreads, 0, s>>>(e, pos, w, prec, d, K, y, h_res, x_next, eps);
   return hipGetLastError();
 }
 
