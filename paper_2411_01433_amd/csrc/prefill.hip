@@ -37,6 +37,8 @@
 // scale (w = fp16(q*s)); the pair order this produces,
 // (e0,e4)(e1,e5)(e2,e6)(e3,e7), is matched by staging the activations in
 // LDS with the same permutation inside every 8 elements.
+#include <type_traits>
+
 #include "moe_internal.h"
 
 namespace moe {
@@ -81,31 +83,31 @@ __device__ inline int perm8(int i) { return i < 4 ? 2 * i : 2 * (i - 4) + 1; }
 // the pass and the 8-column piece t & 7 of every stage; the source rows
 // are resolved once per pass (group row j is token perm[off + j] / K of x,
 // or row off + j of H which is already in group order), then each stage
-// is fetched into registers one stage ahead and written to LDS [row][k]
-// (rows beyond n and columns beyond ld are zero).
+// is fetched into registers ahead of use and written to LDS [row][k].
+// Rows beyond n repeat row n - 1 (row j of a product depends on row j of
+// the activations only, and those rows are not stored) and stages past the
+// end reload stage 0: every load is unconditional, so that no branch hides
+// a load from the compiler's wait counting, which would then wait for all
+// loads in flight (the weight prefetch included) at every stage.
 struct ActStager {
   const f16* row[kStageRowsPerThread];
-  u32x4 v[2][kStageRowsPerThread];  // two stages in flight
+  u32x4 v[3][kStageRowsPerThread];  // up to three stages in flight
 
   __device__ void init(const f16* src, int64_t ld, const int32_t* perm, int off,
                        int j0, int n, int K, bool gather) {
 #pragma unroll
     for (int i = 0; i < kStageRowsPerThread; ++i) {
-      const int r = (threadIdx.x / kPieces) + (kThreads / kPieces) * i;
-      row[i] = nullptr;
-      if (r < n) {
-        const int64_t sr = gather ? perm[off + j0 + r] / K : (int64_t)(off + j0 + r);
-        row[i] = src + sr * ld;
-      }
+      const int r = min((int)(threadIdx.x / kPieces) + (kThreads / kPieces) * i, n - 1);
+      const int64_t sr = gather ? perm[off + j0 + r] / K : (int64_t)(off + j0 + r);
+      row[i] = src + sr * ld;
     }
   }
   template <int SLOT>
   __device__ void fetch(int64_t ld, int64_t k0) {
-    const int64_t col = k0 + (threadIdx.x % kPieces) * 8;
+    const int64_t col = (k0 < ld ? k0 : 0) + (threadIdx.x % kPieces) * 8;
 #pragma unroll
     for (int i = 0; i < kStageRowsPerThread; ++i)
-      v[SLOT][i] = (row[i] && col < ld) ? *reinterpret_cast<const u32x4*>(row[i] + col)
-                                        : u32x4{0, 0, 0, 0};
+      v[SLOT][i] = *reinterpret_cast<const u32x4*>(row[i] + col);
   }
   template <int SLOT, bool PERMUTE>
   __device__ void store(f16* lds) const {
@@ -137,46 +139,69 @@ __device__ inline f16x8 a_frag(const f16* lds, int tt, int s) {
   return *reinterpret_cast<const f16x8*>(lds + (tt * 16 + (l & 15)) * kLdsRow + col);
 }
 
-// Weight fragments of one 16-row tile of one matrix for one stage.
+// Per-lane sources of one matrix M for one pass: the lane's weight row
+// (codes or fp16) and scale row, advanced to its lane group's first column
+// of a stage (fp16: 8g; codes: 16g, one scale per 32 columns).  Resolved
+// once per pass with M a compile-time index, so the expert entry is never
+// indexed at run time (that would put it in scratch memory, and a scratch
+// load makes the wait before it cover every load in flight).
+template <int BITS> struct WRow {
+  const uint8_t* w;
+  const f16* s;
+};
+
+template <int BITS, int M>
+__device__ inline WRow<BITS> wrow(const ExpertEntry& ex, int64_t row, int64_t ld) {
+  const int g = (threadIdx.x & 63) >> 4;
+  WRow<BITS> r;
+  if (BITS == 16) {
+    r.w = reinterpret_cast<const uint8_t*>(ex.w[M] + row * ld + 8 * g);
+    r.s = nullptr;
+  } else {
+    const uint8_t* q = BITS == 8 ? ex.hq[M] : ex.q[M];
+    const f16* sc = BITS == 8 ? ex.hs[M] : ex.s[M];
+    r.w = q + row * (ld * BITS / 8) + 16 * g * BITS / 8;
+    r.s = sc + row * (ld / kGroup) + (g >> 1);
+  }
+  return r;
+}
+
+// Weight fragments of one 16-row tile of one matrix for one stage at
+// column k0 (a multiple of 64).
 template <int BITS> struct WFrag;
 
 template <> struct WFrag<16> {
   u32x4 v[kSteps];
-  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
-                              int64_t ld, int64_t k0) {
-    const int g = (threadIdx.x & 63) >> 4;
+  __device__ inline void load(const WRow<16>& r, int64_t k0) {
 #pragma unroll
-    for (int s = 0; s < kSteps; ++s) {
-      const int64_t col = k0 + 32 * s + 8 * g;
-      v[s] = (ok && col < ld)
-                 ? *gmem(reinterpret_cast<const u32x4*>(ex.w[m] + row * ld + col))
-                 : u32x4{0, 0, 0, 0};
-    }
+    for (int s = 0; s < kSteps; ++s)
+      v[s] = *gmem(reinterpret_cast<const u32x4*>(r.w + 2 * (k0 + 32 * s)));
   }
   __device__ inline f16x8 get(int s) const { return __builtin_bit_cast(f16x8, v[s]); }
 };
 
+// Scales are held zero-extended in a register of their own: packed two to
+// a register, each insertion waits for its load at once.
+__device__ inline f16x2 splat_scale(uint32_t sc) {
+  return as_h2(__builtin_amdgcn_perm(sc, sc, 0x01000100u));
+}
+__device__ inline uint32_t load_scale(const f16* p) {
+  return *gmem(reinterpret_cast<const uint16_t*>(p));
+}
+
 template <> struct WFrag<8> {
   u32x4 q;
-  f16 sc;
+  uint32_t sc;
   // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
-  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
-                              int64_t ld, int64_t k0) {
-    const int g = (threadIdx.x & 63) >> 4;
-    const int64_t col = k0 + 16 * g;
-    if (ok && col < ld) {
-      q = *gmem(reinterpret_cast<const u32x4*>(ex.hq[m] + row * ld + col));
-      sc = *gmem(ex.hs[m] + row * (ld / kGroup) + col / kGroup);
-    } else {
-      q = u32x4{0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u};  // q = 0
-      sc = (f16)0.0f;
-    }
+  __device__ inline void load(const WRow<8>& r, int64_t k0) {
+    q = *gmem(reinterpret_cast<const u32x4*>(r.w + k0));
+    sc = load_scale(r.s + k0 / kGroup);
   }
   // bytes e0..e3 of a word, middle bytes swapped (e0 e2 e1 e3), pair as
   // (e0,e1)(e2,e3) in column order, scaled
   __device__ inline f16x8 get(int s) const {
     const f16x2 bias = as_h2(0x64806480u);  // 1152 = 1024 + 128
-    const f16x2 s2 = {sc, sc};
+    const f16x2 s2 = splat_scale(sc);
     uint32_t o[4];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
@@ -190,25 +215,17 @@ template <> struct WFrag<8> {
 
 template <> struct WFrag<4> {
   u32x2 q;
-  f16 sc;
+  uint32_t sc;
   // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
-  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
-                              int64_t ld, int64_t k0) {
-    const int g = (threadIdx.x & 63) >> 4;
-    const int64_t col = k0 + 16 * g;
-    if (ok && col < ld) {
-      q = *gmem(reinterpret_cast<const u32x2*>(ex.q[m] + row * (ld / 2) + col / 2));
-      sc = *gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup);
-    } else {
-      q = u32x2{0x88888888u, 0x88888888u};  // q = 0
-      sc = (f16)0.0f;
-    }
+  __device__ inline void load(const WRow<4>& r, int64_t k0) {
+    q = *gmem(reinterpret_cast<const u32x2*>(r.w + k0 / 2));
+    sc = load_scale(r.s + k0 / kGroup);
   }
   // word with e0..e7 at bits 4j -> (e0,e4)(e1,e5)(e2,e6)(e3,e7), scaled
   __device__ inline f16x8 get(int s) const {
     const uint32_t w = s == 0 ? q.x : q.y;
     const f16x2 bias = as_h2(0x64086408u);  // 1032 = 1024 + 8
-    const f16x2 s2 = {sc, sc};
+    const f16x2 s2 = splat_scale(sc);
     uint32_t o[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k)
@@ -219,19 +236,11 @@ template <> struct WFrag<4> {
 
 template <> struct WFrag<2> {
   uint32_t q;
-  f16 sc;
+  uint32_t sc;
   // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
-  __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, bool ok,
-                              int64_t ld, int64_t k0) {
-    const int g = (threadIdx.x & 63) >> 4;
-    const int64_t col = k0 + 16 * g;
-    if (ok && col < ld) {
-      q = *gmem(reinterpret_cast<const uint32_t*>(ex.q[m] + row * (ld / 4) + col / 4));
-      sc = *gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup);
-    } else {
-      q = 0xAAAAAAAAu;  // q = 0
-      sc = (f16)0.0f;
-    }
+  __device__ inline void load(const WRow<2>& r, int64_t k0) {
+    q = *gmem(reinterpret_cast<const uint32_t*>(r.w + k0 / 4));
+    sc = load_scale(r.s + k0 / kGroup);
   }
   // half-word s holds e0..e7 at bits 2j; move byte 1 to byte 2 so that the
   // mask 0x00030003 pairs (e_k, e_{k+4})
@@ -239,7 +248,7 @@ template <> struct WFrag<2> {
     const uint32_t w = q >> (16 * s);
     const uint32_t v = (w & 0xFFu) | ((w & 0xFF00u) << 8);
     const f16x2 bias = as_h2(0x64026402u);  // 1026 = 1024 + 2
-    const f16x2 s2 = {sc, sc};
+    const f16x2 s2 = splat_scale(sc);
     uint32_t o[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k)
@@ -250,138 +259,145 @@ template <> struct WFrag<2> {
 
 // One pass (up to kPassTok tokens) of one group over NM matrices:
 // acc[rt][tt][m] accumulates the tokens of tile tt against the weight rows
-// of tile rt.  Software pipeline: while the MFMAs of stage k run, the
-// weight fragments of stage k+2 and the activations of stage k+ADEPTH are
-// in flight (ADEPTH 2: two register slots, used by the down-projection; the
-// up-projection's registers are full).
-template <int BITS, int NM, int RT, int ADEPTH>
-__device__ void gemm_pass(const ExpertEntry& ex, const int (&mats)[NM],
-                          int64_t wrow0, int64_t n_rows, int64_t ld,
+// of tile rt.  Software pipeline over the stages k (64 columns each): the
+// weight fragments sit in a ring of WRING register slots (stage k in slot
+// k % WRING, reloaded with stage k + WRING as soon as its products are
+// issued; 2 slots for the up-projection, 3 for the down-projection) and the activations of stage k + ADEPTH are fetched into
+// register slot k % ADEPTH right after stage k's barrier.  The memory
+// counter completes in order, so a weight load issued before an activation
+// fetch must also be complete when that activation is stored: the weights
+// get about ADEPTH stages to arrive, whatever the ring depth.  ADEPTH is 3
+// for the down-projection and 1 for the up-projection, whose registers
+// are full.  The stage loop is unrolled by kUnroll so that every ring index
+// is static: rotating register slots would copy registers whose loads are
+// still in flight, and make every stage wait for all of them.
+constexpr int kUnroll = 6;  // multiple of WRING (2, 3), ADEPTH (1, 3) and the 2 LDS buffers
+
+// Products of one stage: per token tile, both k-steps' fragments are read
+// from LDS together and feed 2 * RT * NM products, so each LDS round trip
+// is spread over more matrix-core work.
+template <int BITS, int NM, int RT>
+__device__ inline void stage_mma(const f16* cur, const WFrag<BITS> (&w)[RT][NM], int ntile,
+                                 f32x4 (&acc)[RT][kTokTiles][NM]) {
+  f16x8 b[kSteps][RT][NM];
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int m = 0; m < NM; ++m) b[s][rt][m] = w[rt][m].get(s);
+#pragma unroll
+  for (int tt = 0; tt < kTokTiles; ++tt) {
+    // tile 0 always holds a token: every path consumes the weight
+    // registers, so their reload needs no wait for an unconsumed load
+    if (tt == 0 || tt < ntile) {
+      f16x8 a[kSteps];
+#pragma unroll
+      for (int s = 0; s < kSteps; ++s) a[s] = a_frag<BITS>(cur, tt, s);
+#pragma unroll
+      for (int s = 0; s < kSteps; ++s)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int m = 0; m < NM; ++m)
+            acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[s], b[s][rt][m], acc[rt][tt][m], 0, 0, 0);
+    }
+  }
+}
+
+template <int BITS, int M0, int NM, int RT, int ADEPTH, int WRING>
+__device__ void gemm_pass(const ExpertEntry& ex, int64_t wrow0, int64_t ld,
                           const f16* act, int64_t act_ld, const int32_t* perm,
                           int off, int j0, int n, int K, bool gather, f16* lds,
                           f32x4 (&acc)[RT][kTokTiles][NM]) {
+  static_assert(NM == 1 || NM == 2, "one or two matrices");
+  static_assert(kUnroll == 6 && kUnroll % WRING == 0 && kUnroll % ADEPTH == 0, "ring");
   const int l = threadIdx.x & 63;
   const int ntile = (n + 15) >> 4;
+  const int64_t nst = ld / kStageK;  // ld is a multiple of kStageK
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int tt = 0; tt < kTokTiles; ++tt)
 #pragma unroll
       for (int m = 0; m < NM; ++m) acc[rt][tt][m] = f32x4{0, 0, 0, 0};
-  auto load_w = [&](WFrag<BITS> (&w)[RT][NM], int64_t k0) {
+  WRow<BITS> src[RT][NM];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const int64_t row = wrow0 + rt * 16 + (l & 15);
+  for (int rt = 0; rt < RT; ++rt) {
+    const int64_t row = wrow0 + rt * 16 + (l & 15);
+    src[rt][0] = wrow<BITS, M0>(ex, row, ld);
+    if constexpr (NM == 2) src[rt][1] = wrow<BITS, M0 + 1>(ex, row, ld);
+  }
+  // stages past the end reload stage 0 (never multiplied): unconditional
+  // loads, see ActStager
+  auto load_w = [&](WFrag<BITS> (&w)[RT][NM], int64_t k) {
+    const int64_t kc = k < nst ? k * kStageK : 0;
 #pragma unroll
-      for (int m = 0; m < NM; ++m) w[rt][m].load(ex, mats[m], row, row < n_rows, ld, k0);
-    }
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int m = 0; m < NM; ++m) w[rt][m].load(src[rt][m], kc);
   };
   ActStager st;
   st.init(act, act_ld, perm, off, j0, n, K, gather);
   st.fetch<0>(act_ld, 0);
-  WFrag<BITS> w0[RT][NM], w1[RT][NM];
-  load_w(w0, 0);
-  load_w(w1, kStageK);   // masked beyond ld
-  if constexpr (ADEPTH == 1) {
-    int buf = 0;
-    for (int64_t k0 = 0; k0 < ld; k0 += kStageK, buf ^= 1) {
-      f16* cur = lds + buf * (kPassTok * kLdsRow);
-      // the buffer written here was last read two stages ago, before the
-      // previous stage's barrier
-      st.store<0, kPermuted<BITS>>(cur);
-      __syncthreads();
-      if (k0 + kStageK < ld) st.fetch<0>(act_ld, k0 + kStageK);
-      WFrag<BITS> w2[RT][NM];
-      load_w(w2, k0 + 2 * kStageK);
+  if (ADEPTH >= 2) st.fetch<1>(act_ld, kStageK);
+  if (ADEPTH >= 3) st.fetch<2>(act_ld, 2 * kStageK);
+  // issue order as in the loop (activations, then weights), so that the
+  // wait before the first store is the loop's
+  __builtin_amdgcn_sched_barrier(0);
+  WFrag<BITS> w[WRING][RT][NM];
 #pragma unroll
-      for (int s = 0; s < kSteps; ++s) {
-        f16x8 b[RT][NM];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-          for (int m = 0; m < NM; ++m) b[rt][m] = w0[rt][m].get(s);
-#pragma unroll
-        for (int tt = 0; tt < kTokTiles; ++tt) {
-          if (tt < ntile) {
-            const f16x8 a = a_frag<BITS>(cur, tt, s);
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-              for (int m = 0; m < NM; ++m)
-                acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[rt][m], acc[rt][tt][m], 0, 0, 0);
-          }
-        }
-      }
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int m = 0; m < NM; ++m) {
-          w0[rt][m] = w1[rt][m];
-          w1[rt][m] = w2[rt][m];
-        }
-    }
-  } else {
-  st.fetch<1>(act_ld, kStageK);
-  // two stages per iteration: LDS buffers and activation slots alternate
-  for (int64_t k00 = 0; k00 < ld; k00 += 2 * kStageK) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int64_t k0 = k00 + u * kStageK;
-      f16* cur = lds + u * (kPassTok * kLdsRow);
-      // the buffer written here was last read two stages ago, before the
-      // previous stage's barrier; its activations were fetched two stages ago
-      if (u == 0) st.store<0, kPermuted<BITS>>(cur);
-      else st.store<1, kPermuted<BITS>>(cur);
-      __syncthreads();
-      if (u == 0) st.fetch<0>(act_ld, k0 + 2 * kStageK);
-      else st.fetch<1>(act_ld, k0 + 2 * kStageK);
-      WFrag<BITS> w2[RT][NM];
-      load_w(w2, k0 + 2 * kStageK);
-      if (k0 < ld) {
-#pragma unroll
-        for (int s = 0; s < kSteps; ++s) {
-          f16x8 b[RT][NM];
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-            for (int m = 0; m < NM; ++m) b[rt][m] = w0[rt][m].get(s);
-#pragma unroll
-          for (int tt = 0; tt < kTokTiles; ++tt) {
-            if (tt < ntile) {
-              const f16x8 a = a_frag<BITS>(cur, tt, s);
-#pragma unroll
-              for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                for (int m = 0; m < NM; ++m)
-                  acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[rt][m], acc[rt][tt][m], 0, 0, 0);
-            }
-          }
-        }
-      }
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int m = 0; m < NM; ++m) {
-          w0[rt][m] = w1[rt][m];
-          w1[rt][m] = w2[rt][m];
-        }
-    }
+  for (int u = 0; u < WRING; ++u) load_w(w[u], u);
+  // one stage; u = k % kUnroll is a compile-time constant.  The stages of
+  // the main loop are unconditional: a skippable stage would let the
+  // compiler assume its loads missing and wait for every load in flight
+  // (the tail, under kUnroll stages, accepts that).
+  auto stage = [&](int64_t k, auto uc) {
+    constexpr int u = decltype(uc)::value;
+    constexpr int kSlot = u % ADEPTH;
+    // the buffer written here was last read two stages ago, before the
+    // previous stage's barrier
+    f16* cur = lds + (u & 1) * (kPassTok * kLdsRow);
+    st.store<kSlot, kPermuted<BITS>>(cur);
+    __syncthreads();
+    st.fetch<kSlot>(act_ld, (k + ADEPTH) * kStageK);
+    stage_mma<BITS, NM, RT>(cur, w[u % WRING], ntile, acc);
+    load_w(w[u % WRING], k + WRING);
+    // keep stages apart: scheduled across stages, the loads and fragment
+    // reads of later stages stretch the registers' live ranges
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using I5 = std::integral_constant<int, 5>;
+  int64_t k0 = 0;
+  for (; k0 + kUnroll <= nst; k0 += kUnroll) {
+    stage(k0, I0{}); stage(k0 + 1, I1{}); stage(k0 + 2, I2{});
+    stage(k0 + 3, I3{}); stage(k0 + 4, I4{}); stage(k0 + 5, I5{});
   }
-  }
+  // the last nst - k0 < kUnroll stages
+  const int64_t r = nst - k0;
+  if (r > 0) stage(k0, I0{});
+  if (r > 1) stage(k0 + 1, I1{});
+  if (r > 2) stage(k0 + 2, I2{});
+  if (r > 3) stage(k0 + 3, I3{});
+  if (r > 4) stage(k0 + 4, I4{});
   __syncthreads();  // the LDS buffers are reused by the next pass
 }
 
 template <int BITS>
-__device__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* perm,
+__device__ __forceinline__ void up_group(const ExpertEntry& ex, const Group& g, const int32_t* perm,
                          const f16* x, f16* h, int d, int f, int K, int tile, f16* lds) {
   constexpr int RT = kUpRowsW / 16;
   const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t wrow0 = (int64_t)tile * kWaves * kUpRowsW + wave * kUpRowsW;
-  const int mats[2] = {0, 1};
   for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
     const int n = min(kPassTok, g.count - j0);
     f32x4 acc[RT][kTokTiles][2];
-    gemm_pass<BITS, 2, RT, 1>(ex, mats, wrow0, f, d, x, d, perm, g.offset, j0, n, K, true, lds, acc);
+    gemm_pass<BITS, 0, 2, RT, 1, 2>(ex, wrow0, d, x, d, perm, g.offset, j0, n, K, true, lds, acc);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int64_t row = wrow0 + rt * 16 + (l & 15);
@@ -421,16 +437,15 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_up_kernel(
 }
 
 template <int BITS>
-__device__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
+__device__ __forceinline__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
                            float* e, int d, int f, int tile, f16* lds) {
   constexpr int RT = kDownRowsW / 16;
   const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t wrow0 = (int64_t)tile * kWaves * kDownRowsW + wave * kDownRowsW;
-  const int mats[1] = {2};
   for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
     const int n = min(kPassTok, g.count - j0);
     f32x4 acc[RT][kTokTiles][1];
-    gemm_pass<BITS, 1, RT, 2>(ex, mats, wrow0, d, f, h, f, nullptr, g.offset, j0, n, 1, false, lds, acc);
+    gemm_pass<BITS, 2, 1, RT, 3, 3>(ex, wrow0, f, h, f, nullptr, g.offset, j0, n, 1, false, lds, acc);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int64_t row = wrow0 + rt * 16 + (l & 15);
@@ -524,6 +539,8 @@ hipError_t launch_prefill_up(const ExpertEntry* table, const WorkList* wl,
                              const int32_t* perm, const f16* x, f16* h, int T,
                              int d, int f, int K, int max_groups, hipStream_t s) {
   (void)T;
+  // whole stages and whole row tiles: every load stays inside the matrices
+  if (d % kStageK || f % (kWaves * kUpRowsW)) return hipErrorInvalidValue;
   const int rows_per_block = kWaves * kUpRowsW;
   const int n_tiles = (f + rows_per_block - 1) / rows_per_block;
   prefill_up_kernel<<<max_groups * n_tiles, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K, n_tiles);
@@ -535,6 +552,7 @@ hipError_t launch_prefill_down(const ExpertEntry* table, const WorkList* wl,
                                int max_groups, hipStream_t s) {
   (void)T;
   (void)K;
+  if (f % kStageK || d % (kWaves * kDownRowsW)) return hipErrorInvalidValue;
   const int rows_per_block = kWaves * kDownRowsW;
   const int n_tiles = (d + rows_per_block - 1) / rows_per_block;
   prefill_down_kernel<<<max_groups * n_tiles, kThreads, 0, s>>>(table, wl, h, e, d, f, n_tiles);
