@@ -89,25 +89,30 @@ __device__ inline int perm8(int i) { return i < 4 ? 2 * i : 2 * (i - 4) + 1; }
 // end reload stage 0: every load is unconditional, so that no branch hides
 // a load from the compiler's wait counting, which would then wait for all
 // loads in flight (the weight prefetch included) at every stage.
+// Rows are held as 32-bit byte offsets from a block-uniform base (the
+// gathered token rows of x lie within T * d_model halves, a group's rows of
+// H within kPassTok * d_ff), which leaves registers for a deeper ring.
 struct ActStager {
-  const f16* row[kStageRowsPerThread];
+  const char* base;
+  uint32_t row[kStageRowsPerThread];
   u32x4 v[3][kStageRowsPerThread];  // up to three stages in flight
 
   __device__ void init(const f16* src, int64_t ld, const int32_t* perm, int off,
                        int j0, int n, int K, bool gather) {
+    base = reinterpret_cast<const char*>(gather ? src : src + (int64_t)(off + j0) * ld);
 #pragma unroll
     for (int i = 0; i < kStageRowsPerThread; ++i) {
       const int r = min((int)(threadIdx.x / kPieces) + (kThreads / kPieces) * i, n - 1);
-      const int64_t sr = gather ? perm[off + j0 + r] / K : (int64_t)(off + j0 + r);
-      row[i] = src + sr * ld;
+      const int64_t sr = gather ? perm[off + j0 + r] / K : (int64_t)r;
+      row[i] = (uint32_t)((sr * ld + (threadIdx.x % kPieces) * 8) * 2);
     }
   }
   template <int SLOT>
   __device__ void fetch(int64_t ld, int64_t k0) {
-    const int64_t col = (k0 < ld ? k0 : 0) + (threadIdx.x % kPieces) * 8;
+    const char* b = base + 2 * (k0 < ld ? k0 : 0);
 #pragma unroll
     for (int i = 0; i < kStageRowsPerThread; ++i)
-      v[SLOT][i] = *reinterpret_cast<const u32x4*>(row[i] + col);
+      v[SLOT][i] = *reinterpret_cast<const u32x4*>(b + row[i]);
   }
   template <int SLOT, bool PERMUTE>
   __device__ void store(f16* lds) const {
@@ -145,9 +150,12 @@ __device__ inline f16x8 a_frag(const f16* lds, int tt, int s) {
 // once per pass with M a compile-time index, so the expert entry is never
 // indexed at run time (that would put it in scratch memory, and a scratch
 // load makes the wait before it cover every load in flight).
+// Held as block-uniform bases and 32-bit per-lane byte offsets (a matrix
+// is at most 2^30 weights), which the loads take as base + offset.
 template <int BITS> struct WRow {
-  const uint8_t* w;
-  const f16* s;
+  const uint8_t* w;   // block-uniform
+  const uint8_t* s;   // block-uniform
+  uint32_t wo, so;    // this lane's byte offsets
 };
 
 template <int BITS, int M>
@@ -155,13 +163,15 @@ __device__ inline WRow<BITS> wrow(const ExpertEntry& ex, int64_t row, int64_t ld
   const int g = (threadIdx.x & 63) >> 4;
   WRow<BITS> r;
   if (BITS == 16) {
-    r.w = reinterpret_cast<const uint8_t*>(ex.w[M] + row * ld + 8 * g);
+    r.w = reinterpret_cast<const uint8_t*>(ex.w[M]);
+    r.wo = (uint32_t)((row * ld + 8 * g) * 2);
     r.s = nullptr;
+    r.so = 0;
   } else {
-    const uint8_t* q = BITS == 8 ? ex.hq[M] : ex.q[M];
-    const f16* sc = BITS == 8 ? ex.hs[M] : ex.s[M];
-    r.w = q + row * (ld * BITS / 8) + 16 * g * BITS / 8;
-    r.s = sc + row * (ld / kGroup) + (g >> 1);
+    r.w = BITS == 8 ? ex.hq[M] : ex.q[M];
+    r.s = reinterpret_cast<const uint8_t*>(BITS == 8 ? ex.hs[M] : ex.s[M]);
+    r.wo = (uint32_t)(row * (ld * BITS / 8) + 16 * g * BITS / 8);
+    r.so = (uint32_t)((row * (ld / kGroup) + (g >> 1)) * 2);
   }
   return r;
 }
@@ -175,7 +185,7 @@ template <> struct WFrag<16> {
   __device__ inline void load(const WRow<16>& r, int64_t k0) {
 #pragma unroll
     for (int s = 0; s < kSteps; ++s)
-      v[s] = *gmem(reinterpret_cast<const u32x4*>(r.w + 2 * (k0 + 32 * s)));
+      v[s] = *gmem(reinterpret_cast<const u32x4*>(r.w + 2 * (k0 + 32 * s) + r.wo));
   }
   __device__ inline f16x8 get(int s) const { return __builtin_bit_cast(f16x8, v[s]); }
 };
@@ -185,7 +195,7 @@ template <> struct WFrag<16> {
 __device__ inline f16x2 splat_scale(uint32_t sc) {
   return as_h2(__builtin_amdgcn_perm(sc, sc, 0x01000100u));
 }
-__device__ inline uint32_t load_scale(const f16* p) {
+__device__ inline uint32_t load_scale(const uint8_t* p) {
   return *gmem(reinterpret_cast<const uint16_t*>(p));
 }
 
@@ -194,8 +204,8 @@ template <> struct WFrag<8> {
   uint32_t sc;
   // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
   __device__ inline void load(const WRow<8>& r, int64_t k0) {
-    q = *gmem(reinterpret_cast<const u32x4*>(r.w + k0));
-    sc = load_scale(r.s + k0 / kGroup);
+    q = *gmem(reinterpret_cast<const u32x4*>(r.w + k0 + r.wo));
+    sc = load_scale(r.s + 2 * (k0 / kGroup) + r.so);
   }
   // bytes e0..e3 of a word, middle bytes swapped (e0 e2 e1 e3), pair as
   // (e0,e1)(e2,e3) in column order, scaled
@@ -218,8 +228,8 @@ template <> struct WFrag<4> {
   uint32_t sc;
   // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
   __device__ inline void load(const WRow<4>& r, int64_t k0) {
-    q = *gmem(reinterpret_cast<const u32x2*>(r.w + k0 / 2));
-    sc = load_scale(r.s + k0 / kGroup);
+    q = *gmem(reinterpret_cast<const u32x2*>(r.w + k0 / 2 + r.wo));
+    sc = load_scale(r.s + 2 * (k0 / kGroup) + r.so);
   }
   // word with e0..e7 at bits 4j -> (e0,e4)(e1,e5)(e2,e6)(e3,e7), scaled
   __device__ inline f16x8 get(int s) const {
@@ -239,8 +249,8 @@ template <> struct WFrag<2> {
   uint32_t sc;
   // lane group g holds the 16 codes of columns [k0 + 16g, k0 + 16g + 16)
   __device__ inline void load(const WRow<2>& r, int64_t k0) {
-    q = *gmem(reinterpret_cast<const uint32_t*>(r.w + k0 / 4));
-    sc = load_scale(r.s + k0 / kGroup);
+    q = *gmem(reinterpret_cast<const uint32_t*>(r.w + k0 / 4 + r.wo));
+    sc = load_scale(r.s + 2 * (k0 / kGroup) + r.so);
   }
   // half-word s holds e0..e7 at bits 2j; move byte 1 to byte 2 so that the
   // mask 0x00030003 pairs (e_k, e_{k+4})
@@ -262,13 +272,14 @@ template <> struct WFrag<2> {
 // of tile rt.  Software pipeline over the stages k (64 columns each): the
 // weight fragments sit in a ring of WRING register slots (stage k in slot
 // k % WRING, reloaded with stage k + WRING as soon as its products are
-// issued; 2 slots for the up-projection, 3 for the down-projection) and the activations of stage k + ADEPTH are fetched into
-// register slot k % ADEPTH right after stage k's barrier.  The memory
+// issued; 2 slots for the up-projection, 3 for the down-projection) and
+// the activations of stage k + ADEPTH are fetched into register slot
+// k % ADEPTH right after stage k's barrier.  The memory
 // counter completes in order, so a weight load issued before an activation
 // fetch must also be complete when that activation is stored: the weights
 // get about ADEPTH stages to arrive, whatever the ring depth.  ADEPTH is 3
-// for the down-projection and 1 for the up-projection, whose registers
-// are full.  The stage loop is unrolled by kUnroll so that every ring index
+// for the down-projection and 1 for the up-projection (2 fits in its
+// registers but measured no faster).  The stage loop is unrolled by kUnroll so that every ring index
 // is static: rotating register slots would copy registers whose loads are
 // still in flight, and make every stage wait for all of them.
 constexpr int kUnroll = 6;  // multiple of WRING (2, 3), ADEPTH (1, 3) and the 2 LDS buffers
