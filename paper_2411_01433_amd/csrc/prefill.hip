@@ -284,12 +284,16 @@ template <> struct WFrag<2> {
 // still in flight, and make every stage wait for all of them.
 constexpr int kUnroll = 6;  // multiple of WRING (2, 3), ADEPTH (1, 3) and the 2 LDS buffers
 
-// Products of one stage: per token tile, both k-steps' fragments are read
-// from LDS together and feed 2 * RT * NM products, so each LDS round trip
-// is spread over more matrix-core work.
+// Products of one stage, two token tiles at a time: the four fragments
+// of a tile pair (two tiles x two k-steps) are read from LDS together and
+// feed 4 * RT * NM products, ordered so that the products into one
+// accumulator are 2 * RT * NM apart (no stall on the previous result).  A
+// pair is computed whole when its first tile holds tokens: the second
+// tile's rows then repeat the pass's last token and are not stored.
 template <int BITS, int NM, int RT>
 __device__ inline void stage_mma(const f16* cur, const WFrag<BITS> (&w)[RT][NM], int ntile,
                                  f32x4 (&acc)[RT][kTokTiles][NM]) {
+  static_assert(kTokTiles % 2 == 0, "tile pairs");
   f16x8 b[kSteps][RT][NM];
 #pragma unroll
   for (int s = 0; s < kSteps; ++s)
@@ -298,20 +302,25 @@ __device__ inline void stage_mma(const f16* cur, const WFrag<BITS> (&w)[RT][NM],
 #pragma unroll
       for (int m = 0; m < NM; ++m) b[s][rt][m] = w[rt][m].get(s);
 #pragma unroll
-  for (int tt = 0; tt < kTokTiles; ++tt) {
-    // tile 0 always holds a token: every path consumes the weight
+  for (int tp = 0; tp < kTokTiles; tp += 2) {
+    // pair 0 always holds a token: every path consumes the weight
     // registers, so their reload needs no wait for an unconsumed load
-    if (tt == 0 || tt < ntile) {
-      f16x8 a[kSteps];
-#pragma unroll
-      for (int s = 0; s < kSteps; ++s) a[s] = a_frag<BITS>(cur, tt, s);
+    if (tp == 0 || tp < ntile) {
+      f16x8 a[kSteps][2];
 #pragma unroll
       for (int s = 0; s < kSteps; ++s)
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
+        for (int t = 0; t < 2; ++t) a[s][t] = a_frag<BITS>(cur, tp + t, s);
 #pragma unroll
-          for (int m = 0; m < NM; ++m)
-            acc[rt][tt][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[s], b[s][rt][m], acc[rt][tt][m], 0, 0, 0);
+      for (int s = 0; s < kSteps; ++s)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int m = 0; m < NM; ++m)
+              acc[rt][tp + t][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                  a[s][t], b[s][rt][m], acc[rt][tp + t][m], 0, 0, 0);
     }
   }
 }
