@@ -56,7 +56,6 @@ constexpr int kPassTok = 160;             // tokens per pass (10 MFMA tiles)
 constexpr int kTokTiles = kPassTok / 16;
 constexpr int kLdsRow = kStageK + 8;      // halves per staged row (16 B pad)
 constexpr int kUpRowsW = 16;              // weight rows per wave, up-projection
-constexpr int kDownRowsW = 16;            // weight rows per wave, down-projection
 // staging: thread t owns rows (t >> 3) + 32 i of the pass and 8-column piece t & 7
 constexpr int kPieces = kStageK / 8;
 constexpr int kStageRowsPerThread = kPassTok / (kThreads / kPieces);
@@ -456,12 +455,13 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_up_kernel(
   else up_group<2>(ex, g, perm, x, h, d, f, K, tile, lds);
 }
 
-template <int BITS>
+// RT 16-row tiles of W2 per wave, each activation fragment read from LDS
+// serving all of them
+template <int BITS, int RT>
 __device__ __forceinline__ void down_group(const ExpertEntry& ex, const Group& g, const f16* h,
                            float* e, int d, int f, int tile, f16* lds) {
-  constexpr int RT = kDownRowsW / 16;
   const int l = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t wrow0 = (int64_t)tile * kWaves * kDownRowsW + wave * kDownRowsW;
+  const int64_t wrow0 = (int64_t)(tile * kWaves + wave) * (16 * RT);
   for (int j0 = 0; j0 < g.count; j0 += kPassTok) {
     const int n = min(kPassTok, g.count - j0);
     f32x4 acc[RT][kTokTiles][1];
@@ -480,7 +480,12 @@ __device__ __forceinline__ void down_group(const ExpertEntry& ex, const Group& g
   }
 }
 
-__global__ __launch_bounds__(kThreads, 2) void prefill_down_kernel(
+// RT = 2 (32 rows per wave, 128 per block) when d_model allows it: twice
+// the products per LDS fragment read, at one block of 4 waves per compute
+// unit with up to 512 registers each (down-projection of a Mixtral-shaped
+// 512-token layer 284 -> 256 us against RT = 1 at two blocks per unit).
+template <int RT>
+__global__ __launch_bounds__(kThreads, RT == 2 ? 1 : 2) void prefill_down_kernel(
     const ExpertEntry* __restrict__ table, const WorkList* __restrict__ wl,
     const f16* __restrict__ h, float* __restrict__ e, int d, int f, int n_tiles) {
   __shared__ f16 lds[2 * kPassTok * kLdsRow];
@@ -488,10 +493,10 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_down_kernel(
   if (gi >= wl->n_groups) return;
   const Group g = wl->groups[gi];
   const ExpertEntry ex = table[g.expert];
-  if (g.bits == 16) down_group<16>(ex, g, h, e, d, f, tile, lds);
-  else if (g.bits == 8) down_group<8>(ex, g, h, e, d, f, tile, lds);
-  else if (g.bits == 4) down_group<4>(ex, g, h, e, d, f, tile, lds);
-  else down_group<2>(ex, g, h, e, d, f, tile, lds);
+  if (g.bits == 16) down_group<16, RT>(ex, g, h, e, d, f, tile, lds);
+  else if (g.bits == 8) down_group<8, RT>(ex, g, h, e, d, f, tile, lds);
+  else if (g.bits == 4) down_group<4, RT>(ex, g, h, e, d, f, tile, lds);
+  else down_group<2, RT>(ex, g, h, e, d, f, tile, lds);
 }
 
 __device__ inline float wave_sum(float v) {
@@ -572,10 +577,15 @@ hipError_t launch_prefill_down(const ExpertEntry* table, const WorkList* wl,
                                int max_groups, hipStream_t s) {
   (void)T;
   (void)K;
-  if (f % kStageK || d % (kWaves * kDownRowsW)) return hipErrorInvalidValue;
-  const int rows_per_block = kWaves * kDownRowsW;
-  const int n_tiles = (d + rows_per_block - 1) / rows_per_block;
-  prefill_down_kernel<<<max_groups * n_tiles, kThreads, 0, s>>>(table, wl, h, e, d, f, n_tiles);
+  // whole stages and whole row tiles: every load stays inside the matrices
+  if (f % kStageK || d % (kWaves * 16)) return hipErrorInvalidValue;
+  if (d % (kWaves * 32) == 0) {
+    const int n_tiles = d / (kWaves * 32);
+    prefill_down_kernel<2><<<max_groups * n_tiles, kThreads, 0, s>>>(table, wl, h, e, d, f, n_tiles);
+  } else {
+    const int n_tiles = d / (kWaves * 16);
+    prefill_down_kernel<1><<<max_groups * n_tiles, kThreads, 0, s>>>(table, wl, h, e, d, f, n_tiles);
+  }
   return hipGetLastError();
 }
 
