@@ -17,13 +17,14 @@
 // B[8(l/16)+i][l%16] and C[4(l/16)+i][l%16]): M = tokens (A = activations
 // from LDS, up to 160 per pass = 10 tiles), N = weight rows (B = weight
 // rows, each lane's 8 k-values contiguous in memory), K = reduction dim in
-// stages of 64.  A block of 4 waves owns 4 x 16 weight rows; each wave owns
-// 16 rows for all the pass's tokens (up to 160), so every weight element is
-// fetched from HBM once per pass and used by every token of the group, and
-// each staged activation tile serves 64 weight rows.  Activations are
-// double-buffered in LDS (one barrier per stage, the next stage fetched
-// into registers during the MFMAs) and weight fragments are loaded two
-// stages ahead, straight into registers:
+// stages of 64.  A block of 4 waves owns 64 rows of W1 and W3 (16 per wave)
+// in the up-projection and 128 rows of W2 (32 per wave) in the
+// down-projection; each wave covers its rows for all the pass's tokens (up
+// to 160), so every weight element is fetched from HBM once per pass and
+// used by every token of the group.  Activations are double-buffered in
+// LDS (one barrier per stage, later stages fetched into registers ahead of
+// use) and weight fragments go straight into a ring of registers (see
+// gemm_pass for the pipeline):
 //   fp16: lane group g (= l/16) reads 16 B at k = 32s + 8g for step s;
 //   int8: lane group g reads the 16 B of columns 16g..16g+15 of the stage
 //         and step s uses its words 2s, 2s+1;
@@ -45,9 +46,9 @@ namespace moe {
 
 namespace {
 
-// 4 waves per block, two blocks per compute unit: a stage barrier holds
-// only its block's waves, and the other block runs meanwhile (up-projection
-// 528 -> 484 us per Mixtral-shaped 512-token layer against 8-wave blocks).
+// 4 waves per block; two blocks per compute unit in the up-projection, so
+// that a stage barrier holds only its block's waves and the other block
+// runs meanwhile.
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kStageK = 64;               // reduction columns per stage (2 MFMA steps)
