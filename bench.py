@@ -604,27 +604,33 @@ def parity_and_cpu(args, state, out):
                     experts[int(r.idx[t, k])].weights(int(r.prec[t, k]))
     prep_s = time.perf_counter() - t0
     log(f"oracle: timing (budget {args.cpu_seconds}s)")
+    # the sampled steps are checked once and passed over again until the
+    # time budget is spent (a bounded sample of CPU work)
     errs = []
     t0 = time.perf_counter()
-    done = 0
-    for s in range(n_sample):
-        r = O.route(x_h[s], wg16, tags, wl.top_k, wl.t1, wl.t2,
-                    forced_idx=routes[s].idx)
-        r.prec = routes[s].prec
-        y_ref = O.layer_output(x_h[s], experts, r)
-        done += 1
-        errs.append(float(S.normwise(y_h[s], y_ref).max()))
+    done = passes = 0
+    while True:
+        for s in range(n_sample):
+            r = O.route(x_h[s], wg16, tags, wl.top_k, wl.t1, wl.t2,
+                        forced_idx=routes[s].idx)
+            r.prec = routes[s].prec
+            y_ref = O.layer_output(x_h[s], experts, r)
+            done += 1
+            if passes == 0:
+                errs.append(float(S.normwise(y_h[s], y_ref).max()))
+        passes += 1
         if time.perf_counter() - t0 > args.cpu_seconds:
             break
     dt = time.perf_counter() - t0
-    out["parity"] = {"steps_checked": done, "max_normwise_err": max(errs),
+    out["parity"] = {"steps_checked": len(errs), "max_normwise_err": max(errs),
                      "tol": S.TOL, "ok": max(errs) <= S.TOL}
     out["cpu_baseline"] = {
         "value": done * T / dt, "unit": "tokens/s", "cores": blas_threads(),
         "kind": "oracle",
-        "sample": (f"{done} decode steps (token streams 0..{done - 1}) of the same "
-                   f"layer; float64 numpy oracle with the expert copies already "
-                   f"prepared ({prep_s:.1f}s, excluded)"),
+        "sample": (f"{n_sample} decode steps (token streams 0..{n_sample - 1}) of the "
+                   f"same layer, {passes} passes ({done} steps, {dt:.1f}s); float64 "
+                   f"numpy oracle with the expert copies already prepared "
+                   f"({prep_s:.1f}s, excluded)"),
         "seconds": dt, "host": cpu_info()}
 
 
@@ -636,7 +642,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--workload", default="mixtral_layer_decode_t1")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--cpu-tokens", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-pass", action="store_true",
