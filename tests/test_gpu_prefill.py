@@ -76,13 +76,14 @@ def test_prefill_tiny():
 
 
 def test_prefill_tiny_many_tokens_all_tags():
-    """More tokens than one 128-token pass per group; every tag kind."""
-    wl = _edge("prefill_busy", 41, 256, 512, 4, 2, 300,
+    """Groups of more than one 160-token pass at every width (fp16, int4,
+    int2: about 210 tokens each); every tag kind."""
+    wl = _edge("prefill_busy", 41, 256, 512, 4, 2, 420,
                [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4], t1=0.45, t2=1.0)
     rng = np.random.default_rng(11)
-    idx, prec = _check(wl, wl.fixed_tags, rng.standard_normal((300, 256)).astype(np.float16))
+    idx, prec = _check(wl, wl.fixed_tags, rng.standard_normal((420, 256)).astype(np.float16))
     counts = np.bincount(idx.ravel(), minlength=4)
-    assert counts.max() > 128, counts
+    assert counts[:3].min() > 160, counts
 
 
 def test_prefill_ragged_shapes():
