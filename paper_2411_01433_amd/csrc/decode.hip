@@ -231,6 +231,60 @@ __device__ inline void tile_dots(const ExpertEntry& ex, const int (&mats)[NM],
   }
 }
 
+// tile_dots with this wave's chunks in a ring of two register slots: the
+// next chunk's loads are in flight while the current one is multiplied.
+// Every load is unconditional (lanes past the row end load column 0 and
+// skip the products; slots past the wave's last chunk reload it), so the
+// compiler's wait counts stay exact.
+template <int BITS, int NT, int NM, int ROWS>
+__device__ inline void tile_dots_ring(const ExpertEntry& ex, const int (&mats)[NM],
+                                      int64_t row0, int64_t ld,
+                                      const f16* const (&act_rows)[NT],
+                                      float (&acc)[NM][ROWS][NT]) {
+  constexpr int kEpl = Fmt<BITS>::kEpl;
+  constexpr int kChunk = 64 * kEpl;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int n_chunks = (int)((ld + kChunk - 1) / kChunk);
+  const int nw = (n_chunks - wave + kWaves - 1) / kWaves;  // this wave's chunks
+  if (nw <= 0) return;
+  uint32_t a[2][NT][kEpl / 2];
+  Piece<BITS> pc[2][NM][ROWS];
+  auto col_of = [&](int i) {
+    return (int64_t)(wave + min(i, nw - 1) * kWaves) * kChunk + lane * kEpl;
+  };
+  auto load = [&](int sl, int i) {
+    int64_t col = col_of(i);
+    col = col < ld ? col : 0;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) load_act<BITS>(act_rows[t] + col, a[sl][t]);
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r) pc[sl][m][r].load(ex, mats[m], row0 + r, ld, col);
+  };
+  auto dots = [&](int sl, int i) {
+    if (col_of(i) < ld) {
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+          for (int t = 0; t < NT; ++t) acc[m][r][t] = pc[sl][m][r].dot(a[sl][t], acc[m][r][t]);
+    }
+  };
+  load(0, 0);
+  load(1, 1);
+  int i = 0;
+  for (; i + 2 <= nw; i += 2) {
+    dots(0, i);
+    load(0, i + 2);
+    dots(1, i + 1);
+    load(1, i + 3);
+  }
+  if (i < nw) dots(0, i);
+}
+
 // Sum the per-lane partials over the lanes of each wave and then over the
 // waves; afterwards red[kWaves*V + v] (v = (m*ROWS + i)*NT + t) holds the
 // full value.
@@ -319,7 +373,7 @@ __global__ __launch_bounds__(kThreads) void decode_up_kernel(
 }
 
 // ------------------------------------------------- down-proj + combine
-template <int BITS, int NT, int ROWS>
+template <int BITS, int NT, int ROWS, bool RING>
 __device__ void down_tile(const ExpertEntry& ex, const int32_t* pairs, int n,
                           const f16* h, const float* gate_w, int f, int K,
                           int64_t row0, float* red, float* yacc) {
@@ -332,7 +386,12 @@ __device__ void down_tile(const ExpertEntry& ex, const int32_t* pairs, int n,
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[0][i][t] = 0.0f;
   const int mats[1] = {2};
-  tile_dots<BITS, NT, 1, ROWS>(ex, mats, row0, f, rows, acc);
+  // one-token steps, fp16 copies: the two-slot ring fits the 4 waves per
+  // SIMD that keep every block of the step resident; the two-token kernel
+  // would lose a wave, and code groups measured slower with it (int8 W2
+  // 24.9 -> 26.3 us per int8-model step)
+  if constexpr (RING && BITS == 16) tile_dots_ring<BITS, NT, 1, ROWS>(ex, mats, row0, f, rows, acc);
+  else tile_dots<BITS, NT, 1, ROWS>(ex, mats, row0, f, rows, acc);
   block_reduce<1, NT, ROWS>(acc, red);
   const float* fin = red + kWaves * ROWS * NT;
   for (int v = threadIdx.x; v < ROWS * NT; v += kThreads) {
@@ -353,10 +412,10 @@ __device__ void down_group(const ExpertEntry& ex, const int32_t* pairs, int coun
   constexpr int R = DownRows<NTMAX>::value;
   for (int j0 = 0; j0 < count; j0 += NTMAX) {
     const int n = min(NTMAX, count - j0);
-    if (NTMAX == 1 || n <= 1) down_tile<BITS, 1, R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
-    else if (NTMAX == 2 || n <= 2) down_tile<BITS, (NTMAX < 2 ? NTMAX : 2), R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
-    else if (NTMAX == 4 || n <= 4) down_tile<BITS, (NTMAX < 4 ? NTMAX : 4), R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
-    else down_tile<BITS, NTMAX, R>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
+    if (NTMAX == 1 || n <= 1) down_tile<BITS, 1, R, NTMAX == 1>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
+    else if (NTMAX == 2 || n <= 2) down_tile<BITS, (NTMAX < 2 ? NTMAX : 2), R, false>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
+    else if (NTMAX == 4 || n <= 4) down_tile<BITS, (NTMAX < 4 ? NTMAX : 4), R, false>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
+    else down_tile<BITS, NTMAX, R, false>(ex, pairs + j0, n, h, gate_w, f, K, row0, red, yacc);
   }
 }
 
