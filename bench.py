@@ -26,8 +26,9 @@ Counter modes (run under rocprofv3 --pmc; they print one JSON line):
   --pmc-pass           only the warmup + timed decode steps, with the mean
                        algorithmic up-projection bytes of those launches
 The roofline "traffic" field is read from the committed counter summary
-profiles/decode_up_mixtral_t1_pmc.md and is null when the decode kernel
-source has changed since those counters were taken.
+under profiles/ for the workload (decode_up_mixtral_t1_pmc.md for the
+default) and is null when the kernel's source has changed since those
+counters were taken.
 """
 from __future__ import annotations
 
@@ -47,23 +48,40 @@ sys.path.insert(0, os.path.join(ROOT, "tests"))
 
 METRIC = ("MoE-layer decode tokens/s + effective weight GB/s (% of HBM peak), 1 GPU")
 HBM_PEAK_GBPS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
 N_STREAMS = 64
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "decode_up_mixtral_t1_pmc.md")
-UP_KERNEL_SOURCE = os.path.join(ROOT, "paper_2411_01433_amd", "csrc", "decode.hip")
+CSRC = os.path.join(ROOT, "paper_2411_01433_amd", "csrc")
+# Counter summaries of each workload's dominant kernel (profiles/), and the
+# source file that kernel is built from: the recorded traffic is used only
+# while that source is unchanged.
+PMC_SUMMARIES = {
+    "mixtral_layer_decode_t1": ("decode_up_mixtral_t1_pmc.md", "decode.hip"),
+    "mixtral_layer_decode_t8_skew": ("decode_up_mfma_mixtral_t8_skew_pmc.md", "decode_mfma.hip"),
+    "phi_moe_stack32_decode_t4": ("decode_up_mfma_phi_stack32_t4_pmc.md", "decode_mfma.hip"),
+    "mixtral_stack32_prefill_t512": ("prefill_up_mixtral_stack32_t512_pmc.md", "prefill.hip"),
+}
+# arithmetic type of the path: fp16 activations and dequantised weights into
+# fp32 accumulation; the int8-model workload streams int8 / int2 copies
+DTYPE = {"mixtral_int8_layer_decode_t1": "f16 (int8/int2 weights)"}
 
 
-def source_sha256(path=UP_KERNEL_SOURCE):
-    with open(path, "rb") as fh:
+def source_sha256(workload):
+    if workload not in PMC_SUMMARIES:
+        return None
+    src = os.path.join(CSRC, PMC_SUMMARIES[workload][1])
+    with open(src, "rb") as fh:
         return hashlib.sha256(fh.read()).hexdigest()
 
 
 def measured_traffic(workload):
-    """HBM bytes per launch of the up-projection kernel from the committed
-    counter summary: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
-    scaled by what the counter reads for a copy of known size.  None when
-    there is no summary for this workload or the kernel source changed."""
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by
+    what the counter reads for a copy of known size.  None when there is no
+    summary for this workload or the kernel source changed."""
+    if workload not in PMC_SUMMARIES:
+        return None, "no counter summary for this workload"
     try:
-        text = open(PMC_SUMMARY).read()
+        text = open(os.path.join(ROOT, "profiles", PMC_SUMMARIES[workload][0])).read()
     except OSError:
         return None, "no counter summary"
     m = re.search(r"<!-- traffic-json (\{.*?\}) -->", text, re.S)
@@ -72,11 +90,27 @@ def measured_traffic(workload):
     rec = json.loads(m.group(1))
     if rec.get("workload") != workload:
         return None, "counter summary is for another workload"
-    if rec.get("source_sha256") != source_sha256():
-        return None, "decode kernel source changed since the counters were taken"
+    if rec.get("source_sha256") != source_sha256(workload):
+        return None, "kernel source changed since the counters were taken"
     b = (rec["fetch_kib_per_dispatch"] * rec["fetch_factor"]
          + rec["write_kib_per_dispatch"] * rec["write_factor"]) * 1024.0
     return b, "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
+
+
+def event_overhead_us(n=50):
+    """Cost of two HIP event records back to back after a kernel on the
+    current stream (what an empty stage of the library's stage timing
+    measures)."""
+    import torch
+    a = torch.zeros(256, device="cuda")
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(n)]
+    for e0, e1 in pairs:
+        a.add_(1.0)
+        e0.record()
+        e1.record()
+    torch.cuda.synchronize()
+    return float(np.mean([e0.elapsed_time(e1) for e0, e1 in pairs]) * 1e3)
 
 
 def log(*a):
@@ -191,7 +225,7 @@ def run_decode_layer(args):
         ups = [step_bytes(wl, idx_h[i], prec_h[i], tags)[1] for i in range(n_all)]
         return {"mode": "pmc-pass", "workload": wl.name, "launches": n_all,
                 "up_bytes_per_launch_mean": float(np.mean(ups)),
-                "source_sha256": source_sha256()}, None
+                "source_sha256": source_sha256(wl.name)}, None
     per = [step_bytes(wl, idx_h[i], prec_h[i], tags) for i in range(args.warmup, n_all)]
     b_total = float(np.mean([p[0] for p in per]))
     b_up = float(np.mean([p[1] for p in per]))
@@ -248,7 +282,7 @@ def run_decode_layer(args):
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f16", "data": "synthetic",
+        "dtype": DTYPE.get(wl.name, "f16"), "data": "synthetic",
         "config": {"workload": wl.name, "d_model": d, "d_ff": wl.d_ff,
                    "n_experts": wl.n_experts, "top_k": K, "tokens_per_step": T,
                    "layers": 1, "weight_replicas": R, "token_streams": N_STREAMS,
@@ -286,10 +320,11 @@ def stack_bytes_flops(wl, idx, prec, tags_per_layer):
 
 def run_stack(args):
     """32-layer stacks (residual glue between layers): the Phi-MoE-shaped
-    decode stack (4 tokens) or the Mixtral-shaped prefill stack (512)."""
+    decode stack (4 tokens) or the Mixtral-shaped prefill stack (512).  A
+    step is one pass of the whole stack."""
     import torch
     import gpu_support as S
-    from oracle import moe_oracle as O
+    import paper_2411_01433_amd as P
     from synth import configs as C
 
     wl = C.BY_NAME[args.workload]
@@ -303,12 +338,12 @@ def run_stack(args):
         keep.append(w)
         tags_l.append(tags)
         layers.append(S.make_layer(wl, tags, w, max_tokens=T))
-    h0_np = C.hidden_states(wl).astype(np.float32)
-    x0_np = O.rmsnorm(h0_np.astype(np.float64)).astype(np.float16)
-    h0 = torch.from_numpy(h0_np).to(dev)
+    h0 = torch.from_numpy(C.hidden_states(wl).astype(np.float32)).to(dev)
     h = torch.empty_like(h0)
-    xb = [torch.from_numpy(x0_np).to(dev), torch.empty((T, d), dtype=torch.float16, device=dev)]
-    x_first = xb[0].clone()
+    # the first layer's input, by the library's own RMSNorm of the glue
+    x_first = torch.empty((T, d), dtype=torch.float16, device=dev)
+    P.rmsnorm(h0, x_first)
+    xb = [torch.empty_like(x_first), torch.empty_like(x_first)]
     idx = torch.empty((NL, T, K), dtype=torch.int32, device=dev)
     gw = torch.empty((NL, T, K), dtype=torch.float32, device=dev)
     prec = torch.empty((NL, T, K), dtype=torch.int8, device=dev)
@@ -336,7 +371,15 @@ def run_stack(args):
     ev1.record()
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / args.steps
-    b, fl = stack_bytes_flops(wl, idx.cpu().numpy(), prec.cpu().numpy(), tags_l)
+    idx_h, prec_h = idx.cpu().numpy(), prec.cpu().numpy()
+    ups = [step_bytes(wl, idx_h[l], prec_h[l], tags_l[l])[1] for l in range(NL)]
+    if args.pmc_pass:
+        return {"mode": "pmc-pass", "workload": wl.name,
+                "launches": NL * (args.warmup + args.steps),
+                "up_bytes_per_launch_mean": float(np.mean(ups)),
+                "source_sha256": source_sha256(wl.name)}
+    b, fl = stack_bytes_flops(wl, idx_h, prec_h, tags_l)
+    up_flops = [int((prec_h[l] != 2).sum()) * 2 * 2 * d * wl.d_ff for l in range(NL)]
 
     log("stage timing pass")
     for L in layers:
@@ -352,25 +395,94 @@ def run_stack(args):
         calls += n
         L.enable_timing(False)
     stage_us = (tot / max(calls, 1) * 1e3).tolist()
+    ev_us = event_overhead_us()
+    up_us = stage_us[1] - ev_us
+    up_b, up_fl = float(np.mean(ups)), float(np.mean(up_flops))
+    achieved = up_b / (up_us * 1e-6) / 1e9
+    mfma_achieved = up_fl / (up_us * 1e-6) / 1e12
+    traffic, traffic_note = measured_traffic(wl.name)
     t_s = ms * 1e-3
     frac = max(b / 8e12, fl / 2.5e15) / t_s
+    kernel = "prefill_up_kernel" if prefill else (
+        "decode_up_mfma_kernel" if T >= 3 else "decode_up_kernel")
     out = {
         "metric": METRIC, "value": T / t_s, "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f16", "data": "synthetic",
+        "dtype": DTYPE.get(wl.name, "f16"), "data": "synthetic",
         "config": {"workload": wl.name, "d_model": d, "d_ff": wl.d_ff,
                    "n_experts": wl.n_experts, "top_k": K, "tokens_per_step": T,
                    "layers": NL, "mode": wl.mode, "tags": wl.note},
         "effective_weight_GBps": b / t_s / 1e9,
         "pct_hbm_peak": 100.0 * b / t_s / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": b, "flops_per_step": fl,
-        "mfma_util": fl / t_s / 2.5e15 if prefill else None,
+        "mfma_util_step": fl / t_s / 2.5e15 if prefill else None,
         "roofline_step": {"bound": "hbm" if b / 8e12 >= fl / 2.5e15 else "mfma",
                           "frac": frac},
-        "stage_us_per_layer": dict(zip(["route", "up", "down", "rmsnorm"], stage_us)),
+        "stage_us_per_layer": dict(zip(["route", "up", "down", "glue"], stage_us)),
+        "event_overhead_us": ev_us,
+        "roofline": {"bound": "hbm", "kernel": kernel,
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "traffic_source": traffic_note,
+                     "bytes_per_launch": up_b, "mean_launch_us": up_us,
+                     "flops_per_launch": up_fl,
+                     "mfma_achieved_TFLOPs": mfma_achieved,
+                     "mfma_frac": mfma_achieved / MFMA_F16_PEAK_TFLOPS,
+                     "timing": "HIP events between kernels on the launch stream, "
+                               "minus the event-record overhead measured in the same run"},
     }
-    return out
+    return out, (wl, tags_l, layers, x_first, h0, idx, gw, prec)
+
+
+def stack_cpu_baseline(args, state, out):
+    """The oracle streamed one layer at a time on a bounded sample: layer 0
+    of the stack, its first n tokens (the device's own layer input), with
+    the expert copies prepared beforehand (excluded and reported).  Passes
+    over the sample repeat until the time budget is spent; the stack rate
+    is tokens per second through all n_layers layers at that per-layer
+    cost."""
+    import torch
+    import gpu_support as S
+    from oracle import moe_oracle as O
+    from synth import configs as C
+
+    wl, tags_l, layers, x_first, h0, idx, gw, prec = state
+    NL = wl.n_layers
+    n = min(args.cpu_tokens if wl.mode == "prefill" else wl.n_tokens, wl.n_tokens)
+    x_h = x_first.cpu().numpy()[:n]
+    h_h = h0.cpu().numpy()[:n].astype(np.float64)
+    tags = tags_l[0]
+    wg16 = C.router_weight(wl, 0)
+    experts = S.HostExperts(wl, 0, tags)
+    log(f"oracle: preparing the experts layer 0 uses for {n} tokens")
+    t0 = time.perf_counter()
+    r0 = O.route(x_h, wg16, tags, wl.top_k, wl.t1, wl.t2)
+    for t in range(n):
+        for k in range(wl.top_k):
+            if r0.prec[t, k] != O.PREC_SKIP:
+                experts[int(r0.idx[t, k])].weights(int(r0.prec[t, k]))
+    prep_s = time.perf_counter() - t0
+    log(f"oracle: timing (budget {args.cpu_seconds}s)")
+    t0 = time.perf_counter()
+    done = passes = 0
+    while True:
+        r = O.route(x_h, wg16, tags, wl.top_k, wl.t1, wl.t2)
+        y = O.layer_output(x_h, experts, r)
+        O.residual_step(h_h, y, O.RMS_EPS)
+        done += n
+        passes += 1
+        if time.perf_counter() - t0 > args.cpu_seconds:
+            break
+    dt = time.perf_counter() - t0
+    out["cpu_baseline"] = {
+        "value": done / dt / NL, "unit": "tokens/s", "cores": blas_threads(),
+        "kind": "oracle",
+        "sample": (f"layer 0 of the {NL}-layer stack, its first {n} tokens (gate, top-k, "
+                   f"Eq. 2, experts, residual glue), {passes} passes ({done} token-layers, "
+                   f"{dt:.1f}s); rate scaled to all {NL} layers; float64 numpy oracle with the "
+                   f"expert copies already prepared ({prep_s:.1f}s, excluded)"),
+        "seconds": dt, "host": cpu_info()}
 
 
 def run_predictor(args):
@@ -689,7 +801,9 @@ def main():
         print(json.dumps(run_loading(args)), flush=True)
         return
     if C.BY_NAME[args.workload].n_layers > 1:
-        out = run_stack(args)
+        out, state = run_stack(args)
+        if not args.no_cpu_baseline and not args.pmc_pass:
+            stack_cpu_baseline(args, state, out)
         print(json.dumps(out), flush=True)
         return
     out, state = run_decode_layer(args)

@@ -160,6 +160,14 @@ moe_status moe_prefill_residual(moe_layer_t layer, int32_t n_tokens,
                                 int32_t* topk_idx, float* topk_w,
                                 int8_t* prec_used, void* stream);
 
+/* The RMSNorm of the residual glue on its own, to form the first layer's
+ * input of a stack:  x[t] = fp16(h[t] / sqrt(mean_j h[t,j]^2 + eps)), no gain.
+ *  h  device fp32 [n_tokens, d_model];  x  device fp16 [n_tokens, d_model]
+ *  n_tokens >= 1; d_model a positive multiple of 64, <= 16384; eps >= 0.
+ *  Needs no handle; pointers 16-byte aligned. */
+moe_status moe_rmsnorm(const float* h, void* x, int32_t n_tokens, int32_t d_model,
+                       float eps, void* stream);
+
 /* Copy an expert's quantised copy out (for inspection and parity).
  *  matrix  0 = W1, 1 = W3, 2 = W2;  bits 8, 4 or 2 (the copy must exist)
  *  codes   device u8 [rows, cols*bits/8];  scales device fp16 [rows, cols/32]

@@ -9,5 +9,5 @@ from .binding import (  # noqa: F401
     EXPORTED, LIB_PATH, MOE_EHIP, MOE_EINVAL, MOE_ENOMEM, MOE_ESTATE,
     MOE_EUNSUPPORTED, MOE_OK, PREC_HIGH, PREC_LOW, PREC_SKIP, TAG_FP16,
     TAG_INT2, TAG_INT4, TAG_MISS_INT2, TAG_MISS_INT4, LayerDesc, MoeError,
-    MoeCache, MoeLayer, MoePredictor, MoeStore, lib, quantize,
+    MoeCache, MoeLayer, MoePredictor, MoeStore, lib, quantize, rmsnorm,
 )

@@ -29,7 +29,7 @@ EXPORTED = (
     "moe_cache_clear_masks", "moe_cache_replay", "moe_cache_layer_tags",
     "moe_cache_stats", "moe_cache_destroy",
     "moe_store_create", "moe_store_sizes", "moe_store_put", "moe_store_load",
-    "moe_store_destroy", "moe_layer_bind_expert",
+    "moe_store_destroy", "moe_layer_bind_expert", "moe_rmsnorm",
 )
 
 
@@ -112,6 +112,7 @@ def lib() -> ctypes.CDLL:
     L.moe_store_destroy.argtypes = [vp]
     L.moe_layer_bind_expert.argtypes = [vp, i32, i32, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                         ctypes.POINTER(vp), i32, vp]
+    L.moe_rmsnorm.argtypes = [vp, vp, i32, i32, ctypes.c_float, vp]
     L.moe_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
         if name != "moe_last_error":
@@ -155,6 +156,14 @@ def quantize(w, bits: int, codes, scales, stream=None):
         _ptr(w, torch.float16, None, "w"), rows, cols, bits,
         _ptr(codes, torch.uint8, (rows, cols * bits // 8), "codes"),
         _ptr(scales, torch.float16, (rows, cols // 32), "scales"), _stream(stream)))
+
+
+def rmsnorm(h, x, eps: float = 1e-5, stream=None):
+    """x = fp16(rmsnorm(h)) row by row (h fp32 [T, d], x fp16 [T, d])."""
+    import torch
+    T, d = h.shape
+    _check(lib().moe_rmsnorm(_ptr(h, torch.float32, None, "h"),
+                             _ptr(x, torch.float16, (T, d), "x"), T, d, eps, _stream(stream)))
 
 
 class MoeLayer:

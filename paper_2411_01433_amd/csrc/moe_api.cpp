@@ -70,16 +70,12 @@ struct moe_layer {
   std::vector<void*> owned;
   std::vector<std::array<std::array<uint8_t*, 3>, 3>> low_q;
   std::vector<std::array<std::array<f16*, 3>, 3>> low_s;
+  // the fp16 matrix each copy was quantised from (an expert re-bound to
+  // other fp16 weights gets its copies rebuilt)
+  std::vector<std::array<std::array<const f16*, 3>, 3>> low_src;
   // device memory
   ExpertEntry* d_table = nullptr;
-  WorkList* d_wl = nullptr;
-  int32_t* d_perm = nullptr;
-  int32_t* d_pos = nullptr;
-  int32_t* d_idx = nullptr;
-  float* d_w = nullptr;
-  int8_t* d_prec = nullptr;
-  f16* d_h = nullptr;       // [max_tokens*K, f]
-  float* d_eperm = nullptr; // per-pair expert outputs in group order: [max_tokens*K, d]
+  Workspace ws;             // carved from the arena, sized for max_tokens
   void* arena = nullptr;
   // stage timing (measurement only): 5 events per recorded call
   bool timing = false;
@@ -146,11 +142,11 @@ RouteParams route_params(moe_layer* l, int T, const void* x) {
   return p;
 }
 
-RouteOut route_out(moe_layer* l, int32_t* idx, float* w, int8_t* prec) {
+RouteOut route_out(const Workspace& ws, int32_t* idx, float* w, int8_t* prec) {
   RouteOut o;
-  o.idx = l->d_idx;
-  o.w = l->d_w;
-  o.prec = l->d_prec;
+  o.idx = ws.idx;
+  o.w = ws.w;
+  o.prec = ws.prec;
   o.user_idx = idx;
   o.user_w = w;
   o.user_prec = prec;
@@ -180,6 +176,44 @@ hipError_t mark(moe_layer* l, int slot, hipStream_t s) {
 
 constexpr int kDecodeMfmaMinTokens = 3;
 
+// The launch sequence of a decode step with the workspace `ws` (the layer's
+// arena, or the static scratch of the allocation-free entry point).
+moe_status decode_launch(moe_layer* l, const Workspace& ws, int32_t T, const void* x, float* y,
+                         float* h_res, void* x_next, int32_t* idx, float* w, int8_t* prec,
+                         hipStream_t s) {
+  const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
+  const int mg = max_groups_of(l, T);
+  HIP_TRY(mark(l, 0, s), "timing event");
+  HIP_TRY(launch_route_decode(route_params(l, T, x), route_out(ws, idx, w, prec),
+                              ws.wl, ws.perm, ws.pos, s), "route kernel launch");
+  HIP_TRY(mark(l, 1, s), "timing event");
+  if (T >= kDecodeMfmaMinTokens) {
+    // several tokens per step: matrix-core kernels, per-pair down rows and
+    // the fused combine (+ residual rmsnorm) of the prefill path
+    HIP_TRY(launch_decode_up_mfma(l->d_table, ws.wl, ws.perm, static_cast<const f16*>(x),
+                                  ws.h, d, f, K, mg, s), "up kernel launch");
+    HIP_TRY(mark(l, 2, s), "timing event");
+    HIP_TRY(launch_decode_down_mfma(l->d_table, ws.wl, ws.perm, ws.h, ws.eperm,
+                                    d, f, mg, s), "down kernel launch");
+    HIP_TRY(launch_combine_prefill(ws.eperm, ws.pos, ws.w, ws.prec, T, d, K, y, h_res,
+                                   static_cast<f16*>(x_next), l->desc.rms_eps, s),
+            "combine kernel launch");
+    HIP_TRY(mark(l, 3, s), "timing event");
+  } else {
+    HIP_TRY(launch_decode_up(l->d_table, ws.wl, ws.perm, static_cast<const f16*>(x),
+                             ws.h, T, d, f, K, mg, s), "up kernel launch");
+    HIP_TRY(mark(l, 2, s), "timing event");
+    HIP_TRY(launch_decode_down(l->d_table, ws.wl, ws.perm, ws.w, ws.h, y, h_res,
+                               T, d, f, K, s), "down kernel launch");
+    HIP_TRY(mark(l, 3, s), "timing event");
+    if (h_res)
+      HIP_TRY(launch_rmsnorm(h_res, static_cast<f16*>(x_next), T, d, l->desc.rms_eps, s),
+              "rmsnorm kernel launch");
+  }
+  HIP_TRY(mark(l, 4, s), "timing event");
+  return MOE_OK;
+}
+
 moe_status decode_impl(moe_layer* l, int32_t T, const void* x, float* y,
                        float* h_res, void* x_next, int32_t* idx, float* w,
                        int8_t* prec, void* stream) {
@@ -189,38 +223,8 @@ moe_status decode_impl(moe_layer* l, int32_t T, const void* x, float* y,
   if (st != MOE_OK) return st;
   if (h_res && !x_next) return fail(MOE_EINVAL, "x_next must not be NULL");
   if ((st = set_device(l)) != MOE_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
-  const int mg = max_groups_of(l, T);
-  HIP_TRY(mark(l, 0, s), "timing event");
-  HIP_TRY(launch_route_decode(route_params(l, T, x), route_out(l, idx, w, prec),
-                              l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
-  HIP_TRY(mark(l, 1, s), "timing event");
-  if (T >= kDecodeMfmaMinTokens) {
-    // several tokens per step: matrix-core kernels, per-pair down rows and
-    // the fused combine (+ residual rmsnorm) of the prefill path
-    HIP_TRY(launch_decode_up_mfma(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
-                                  l->d_h, d, f, K, mg, s), "up kernel launch");
-    HIP_TRY(mark(l, 2, s), "timing event");
-    HIP_TRY(launch_decode_down_mfma(l->d_table, l->d_wl, l->d_perm, l->d_h, l->d_eperm,
-                                    d, f, mg, s), "down kernel launch");
-    HIP_TRY(launch_combine_prefill(l->d_eperm, l->d_pos, l->d_w, l->d_prec, T, d, K, y, h_res,
-                                   static_cast<f16*>(x_next), l->desc.rms_eps, s),
-            "combine kernel launch");
-    HIP_TRY(mark(l, 3, s), "timing event");
-  } else {
-    HIP_TRY(launch_decode_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
-                             l->d_h, T, d, f, K, mg, s), "up kernel launch");
-    HIP_TRY(mark(l, 2, s), "timing event");
-    HIP_TRY(launch_decode_down(l->d_table, l->d_wl, l->d_perm, l->d_w, l->d_h, y, h_res,
-                               T, d, f, K, s), "down kernel launch");
-    HIP_TRY(mark(l, 3, s), "timing event");
-    if (h_res)
-      HIP_TRY(launch_rmsnorm(h_res, static_cast<f16*>(x_next), T, d, l->desc.rms_eps, s),
-              "rmsnorm kernel launch");
-  }
-  HIP_TRY(mark(l, 4, s), "timing event");
-  return MOE_OK;
+  return decode_launch(l, l->ws, T, x, y, h_res, x_next, idx, w, prec,
+                       static_cast<hipStream_t>(stream));
 }
 
 moe_status prefill_impl(moe_layer* l, int32_t T, const void* x, float* y,
@@ -236,16 +240,17 @@ moe_status prefill_impl(moe_layer* l, int32_t T, const void* x, float* y,
   const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
   const int mg = max_groups_of(l, T);
   HIP_TRY(mark(l, 0, s), "timing event");
-  HIP_TRY(launch_route_prefill(route_params(l, T, x), route_out(l, idx, w, prec),
-                               l->d_wl, l->d_perm, l->d_pos, s), "route kernel launch");
+  const Workspace& ws = l->ws;
+  HIP_TRY(launch_route_prefill(route_params(l, T, x), route_out(ws, idx, w, prec),
+                               ws.wl, ws.perm, ws.pos, s), "route kernel launch");
   HIP_TRY(mark(l, 1, s), "timing event");
-  HIP_TRY(launch_prefill_up(l->d_table, l->d_wl, l->d_perm, static_cast<const f16*>(x),
-                            l->d_h, T, d, f, K, mg, s), "prefill up launch");
+  HIP_TRY(launch_prefill_up(l->d_table, ws.wl, ws.perm, static_cast<const f16*>(x),
+                            ws.h, T, d, f, K, mg, s), "prefill up launch");
   HIP_TRY(mark(l, 2, s), "timing event");
-  HIP_TRY(launch_prefill_down(l->d_table, l->d_wl, l->d_h, l->d_eperm, T, d, f, K, mg, s),
+  HIP_TRY(launch_prefill_down(l->d_table, ws.wl, ws.h, ws.eperm, T, d, f, K, mg, s),
           "prefill down launch");
   HIP_TRY(mark(l, 3, s), "timing event");
-  HIP_TRY(launch_combine_prefill(l->d_eperm, l->d_pos, l->d_w, l->d_prec, T, d, K, y,
+  HIP_TRY(launch_combine_prefill(ws.eperm, ws.pos, ws.w, ws.prec, T, d, K, y,
                                  h_res, static_cast<f16*>(x_next), l->desc.rms_eps, s),
           "combine kernel launch");
   HIP_TRY(mark(l, 4, s), "timing event");
@@ -431,6 +436,7 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   l->host_table.resize(E);
   l->low_q.resize(E);
   l->low_s.resize(E);
+  l->low_src.resize(E);
   for (int e = 0; e < E; ++e) {
     ExpertEntry& x = l->host_table[e];
     std::memset(&x, 0, sizeof x);
@@ -441,6 +447,7 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
     x.hi_bits = 16;
     for (auto& a : l->low_q[e]) a.fill(nullptr);
     for (auto& a : l->low_s[e]) a.fill(nullptr);
+    for (auto& a : l->low_src[e]) a.fill(nullptr);
   }
   // one arena: every region 256-byte aligned
   auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
@@ -461,18 +468,18 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   }
   char* base = static_cast<char*>(l->arena);
   l->d_table = reinterpret_cast<ExpertEntry*>(base + o_table);
-  l->d_wl = reinterpret_cast<WorkList*>(base + o_wl);
-  l->d_perm = reinterpret_cast<int32_t*>(base + o_perm);
-  l->d_pos = reinterpret_cast<int32_t*>(base + o_pos);
-  l->d_idx = reinterpret_cast<int32_t*>(base + o_idx);
-  l->d_w = reinterpret_cast<float*>(base + o_w);
-  l->d_prec = reinterpret_cast<int8_t*>(base + o_prec);
-  l->d_h = reinterpret_cast<f16*>(base + o_h);
-  l->d_eperm = reinterpret_cast<float*>(base + o_ep);
+  l->ws.wl = reinterpret_cast<WorkList*>(base + o_wl);
+  l->ws.perm = reinterpret_cast<int32_t*>(base + o_perm);
+  l->ws.pos = reinterpret_cast<int32_t*>(base + o_pos);
+  l->ws.idx = reinterpret_cast<int32_t*>(base + o_idx);
+  l->ws.w = reinterpret_cast<float*>(base + o_w);
+  l->ws.prec = reinterpret_cast<int8_t*>(base + o_prec);
+  l->ws.h = reinterpret_cast<f16*>(base + o_h);
+  l->ws.eperm = reinterpret_cast<float*>(base + o_ep);
   hipStream_t s = static_cast<hipStream_t>(stream);
   he = hipMemcpyAsync(l->d_table, l->host_table.data(), sizeof(ExpertEntry) * E,
                       hipMemcpyHostToDevice, s);
-  if (he == hipSuccess) he = hipMemsetAsync(l->d_wl, 0, sizeof(WorkList), s);
+  if (he == hipSuccess) he = hipMemsetAsync(l->ws.wl, 0, sizeof(WorkList), s);
   if (he == hipSuccess) he = hipStreamSynchronize(s);
   if (he != hipSuccess) {
     free_layer(l);
@@ -500,29 +507,50 @@ moe_status moe_set_expert_precision(moe_layer_t l, int32_t expert, int32_t tag,
   if (!v.w[0] || !v.w[1] || !v.w[2])
     return fail(MOE_ESTATE, "expert %d is bound without fp16 weights: bind it again instead", expert);
   v.tag = tag;
-  // quantised copies this tag needs, built once from the fp16 weights
+  // quantised copies this tag needs, built once from the fp16 weights (and
+  // rebuilt in place, in stream order, when the expert has been re-bound to
+  // other fp16 weights since)
   const int d = l->desc.d_model, f = l->desc.d_ff;
   auto ensure = [&](int bits, const uint8_t* (&q_out)[3], const f16* (&s_out)[3]) -> moe_status {
     const int slot = slot_of_bits(bits);
     for (int m = 0; m < 3; ++m) {
       const int64_t rows = m < 2 ? f : d, cols = m < 2 ? d : f;
-      if (!l->low_q[expert][slot][m]) {
-        void *q = nullptr, *sc = nullptr;
-        hipError_t he = hipMalloc(&q, (size_t)rows * cols * bits / 8);
-        if (he == hipSuccess) he = hipMalloc(&sc, (size_t)rows * (cols / kGroup) * sizeof(f16));
+      uint8_t* q = l->low_q[expert][slot][m];
+      f16* sc = l->low_s[expert][slot][m];
+      const bool fresh = q == nullptr;
+      if (fresh) {
+        void *qv = nullptr, *sv = nullptr;
+        hipError_t he = hipMalloc(&qv, (size_t)rows * cols * bits / 8);
+        if (he == hipSuccess) he = hipMalloc(&sv, (size_t)rows * (cols / kGroup) * sizeof(f16));
         if (he != hipSuccess) {
-          if (q) (void)hipFree(q);
+          if (qv) (void)hipFree(qv);
           return fail(MOE_ENOMEM, "allocation of the int%d copy failed: %s", bits, hipGetErrorString(he));
         }
-        l->owned.push_back(q);
-        l->owned.push_back(sc);
-        l->low_q[expert][slot][m] = static_cast<uint8_t*>(q);
-        l->low_s[expert][slot][m] = static_cast<f16*>(sc);
-        HIP_TRY(launch_quantize(v.w[m], rows, cols, bits, static_cast<uint8_t*>(q),
-                                static_cast<f16*>(sc), s), "quantize kernel launch");
+        q = static_cast<uint8_t*>(qv);
+        sc = static_cast<f16*>(sv);
       }
-      q_out[m] = l->low_q[expert][slot][m];
-      s_out[m] = l->low_s[expert][slot][m];
+      if (fresh || l->low_src[expert][slot][m] != v.w[m]) {
+        const hipError_t he = launch_quantize(v.w[m], rows, cols, bits, q, sc, s);
+        if (he != hipSuccess) {
+          if (fresh) {
+            (void)hipFree(q);
+            (void)hipFree(sc);
+          } else {
+            // the old contents may be partly overwritten: never reuse them
+            l->low_src[expert][slot][m] = nullptr;
+          }
+          return hip_fail(he, "quantize kernel launch");
+        }
+        if (fresh) {
+          l->owned.push_back(q);
+          l->owned.push_back(sc);
+          l->low_q[expert][slot][m] = q;
+          l->low_s[expert][slot][m] = sc;
+        }
+        l->low_src[expert][slot][m] = v.w[m];
+      }
+      q_out[m] = q;
+      s_out[m] = sc;
     }
     return MOE_OK;
   };
@@ -647,6 +675,20 @@ moe_status moe_quantize(const void* w, int64_t rows, int64_t cols, int32_t bits,
   HIP_TRY(launch_quantize(static_cast<const f16*>(w), rows, cols, bits,
                           static_cast<uint8_t*>(codes), static_cast<f16*>(scales),
                           static_cast<hipStream_t>(stream)), "quantize kernel launch");
+  return MOE_OK;
+}
+
+moe_status moe_rmsnorm(const float* h, void* x, int32_t n_tokens, int32_t d_model, float eps,
+                       void* stream) {
+  g_err.clear();
+  if (!h || !x) return fail(MOE_EINVAL, "h and x must not be NULL");
+  if (n_tokens < 1) return fail(MOE_EINVAL, "n_tokens must be >= 1 (got %d)", n_tokens);
+  if (d_model <= 0 || d_model % 64 || d_model > 16384)
+    return fail(MOE_EINVAL, "d_model must be a positive multiple of 64, <= 16384 (got %d)", d_model);
+  if (!(eps >= 0.0f)) return fail(MOE_EINVAL, "eps must be >= 0");
+  if (!aligned16(h) || !aligned16(x)) return fail(MOE_EINVAL, "h and x must be 16-byte aligned");
+  HIP_TRY(launch_rmsnorm(h, static_cast<f16*>(x), n_tokens, d_model, eps,
+                         static_cast<hipStream_t>(stream)), "rmsnorm kernel launch");
   return MOE_OK;
 }
 

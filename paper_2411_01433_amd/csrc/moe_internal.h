@@ -56,6 +56,20 @@ struct WorkList {
   Group groups[kMaxKeys];
 };
 
+// Device workspace of one layer call: the work list, the pair permutation
+// and its inverse, the routing outputs, the SwiGLU activations h of every
+// pair and the per-pair expert outputs (prefill and matrix-core decode).
+struct Workspace {
+  WorkList* wl = nullptr;
+  int32_t* perm = nullptr;   // [T*K] pairs sorted by work group (stable)
+  int32_t* pos = nullptr;    // [T*K] position of each pair in that order, -1 if skipped
+  int32_t* idx = nullptr;    // [T*K]
+  float* w = nullptr;        // [T*K]
+  int8_t* prec = nullptr;    // [T*K]
+  f16* h = nullptr;          // [T*K, d_ff]
+  float* eperm = nullptr;    // [T*K, d_model] in group order
+};
+
 // Routing outputs of one call; optional user copies may be null.
 struct RouteOut {
   int32_t* idx;        // [T*K] internal

@@ -30,6 +30,12 @@ def device_layer_weights(wl: C.Workload, layer: int, device="cuda"):
     return wg, mats["w1"], mats["w3"], mats["w2"]
 
 
+def rmsnorm_device(h, x):
+    """The library's RMSNorm of the residual glue: x = fp16(rmsnorm(h))."""
+    import paper_2411_01433_amd as P
+    P.rmsnorm(h, x, O.RMS_EPS)
+
+
 def make_layer(wl: C.Workload, tags, weights, max_tokens=None, t1=None, t2=None):
     import paper_2411_01433_amd as P
     wg, w1, w3, w2 = weights

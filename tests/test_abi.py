@@ -112,6 +112,17 @@ def test_quantize_rejects_bad_args():
     assert L.moe_quantize(p, 4, 32, 4, ctypes.c_void_p(0x1008), p, None) == B.MOE_EINVAL
 
 
+def test_rmsnorm_rejects_bad_args():
+    L = B.lib()
+    p = ctypes.c_void_p(0x1000)
+    assert L.moe_rmsnorm(None, p, 4, 64, 1e-5, None) == B.MOE_EINVAL
+    assert L.moe_rmsnorm(p, p, 0, 64, 1e-5, None) == B.MOE_EINVAL
+    assert L.moe_rmsnorm(p, p, 4, 96, 1e-5, None) == B.MOE_EINVAL
+    assert L.moe_rmsnorm(p, p, 4, 64, -1.0, None) == B.MOE_EINVAL
+    assert L.moe_rmsnorm(ctypes.c_void_p(0x1004), p, 4, 64, 1e-5, None) == B.MOE_EINVAL
+    assert b"aligned" in L.moe_last_error()
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "_lib", None)
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))

@@ -57,12 +57,16 @@ def _check(wl, tags, x16, sample=None, t1=None, t2=None, residual=False):
     else:
         out, idx, w, prec = run_prefill(L, x16, d, K)
     L.destroy()
-    rows = np.arange(len(x16)) if sample is None else np.asarray(sample)
+    # routing of every token; the fp64 expert FFN on the sampled rows
     wg16 = C.router_weight(wl, 0)
-    r, _ = S.check_routing(x16[rows], wg16, tags, K, t1, t2, idx[rows], w[rows], prec[rows])
+    r_all, flags = S.check_routing(x16, wg16, tags, K, t1, t2, idx, w, prec)
+    rows = np.arange(len(x16)) if sample is None else np.asarray(sample)
+    r = O.Routing(idx=r_all.idx[rows], w=r_all.w[rows], prec=r_all.prec[rows],
+                  logits=r_all.logits[rows])
     y_ref = O.layer_output(x16[rows], S.HostExperts(wl, 0, tags), r)
     err = S.normwise(out[rows], y_ref)
-    print(f"{wl.name}: max normwise err {err.max():.3e} over {len(rows)} tokens")
+    print(f"{wl.name}: routing exact on {len(x16)} tokens ({len(flags)} flagged near-ties); "
+          f"max normwise err {err.max():.3e} over {len(rows)} tokens")
     assert err.max() <= S.TOL
     if residual:
         h_ref = h0[rows].astype(np.float64) + y_ref
@@ -104,7 +108,8 @@ def test_prefill_skip_and_residual():
 
 def test_prefill_mixtral_layer_t512():
     """One Mixtral-shaped layer of the 512-token prefill workload (4:3:1
-    map of layer 0), 32 sampled tokens checked against the oracle."""
+    map of layer 0): routing of all 512 tokens, the layer output on 32
+    sampled tokens, against the oracle."""
     wl = C.MIXTRAL_PREFILL
     tags = C.layer_tags(wl, 0)
     x = C.hidden_states(wl)

@@ -1,10 +1,16 @@
-"""32-layer stacks with the pre-norm residual glue between layers, checked
-teacher-forced: the whole stack runs on the device, and at sampled layers
-the oracle takes the device's own layer input (x_l, h_l) and must reproduce
-that layer's routing, its increment y_l = h_{l+1} - h_l and the next input
-x_{l+1} = fp16(rmsnorm(h_{l+1})).  Free-running agreement over 32 layers is
-not a parity bar: top-k is discontinuous, so a near-tie in one layer may
-legitimately send the two runs down different experts afterwards."""
+"""32-layer stacks with the pre-norm residual glue between layers.
+
+The whole stack runs on the device once.  Every layer's input x_l and its
+routing outputs (top-k indices, gate values, Eq. 2 precisions) are kept,
+and the routing of EVERY token of EVERY layer is checked against the
+oracle taking the device's own x_l (teacher-forced): indices and
+precisions exact up to the flagged near-ties of the comparison rules, gate
+values within 1e-5.  The fp64 expert FFN is expensive, so the layer output
+(the increment y_l = h_{l+1} - h_l and the next input x_{l+1} =
+fp16(rmsnorm(h_{l+1}))) is checked at sampled layers and tokens.
+Free-running agreement over 32 layers is not a parity bar: top-k is
+discontinuous, so a near-tie in one layer may legitimately send the two
+runs down different experts afterwards."""
 import gc
 
 import numpy as np
@@ -29,88 +35,107 @@ def _need_gpu():
     yield
 
 
-def _run_stack(wl, check_layers):
-    """Run the stack once; return per checked layer the device's
-    (x_l, h_l, h_{l+1}, x_{l+1}, idx, w, prec) on the host."""
+def _run_stack(wl, ffn_layers):
+    """Run the stack once.  Returns every layer's device input x_l and
+    routing (idx, w, prec) on the host, and for the layers in ffn_layers
+    the residual stream before and after the layer."""
     T, K, d, NL = wl.n_tokens, wl.top_k, wl.d_model, wl.n_layers
     layers, keep = [], []
     for l in range(NL):
         w = S.device_layer_weights(wl, l)
         keep.append(w)
         layers.append(S.make_layer(wl, C.layer_tags(wl, l), w, max_tokens=T))
-    h0 = C.hidden_states(wl).astype(np.float32)
-    h = torch.from_numpy(h0).cuda()
-    xb = [torch.from_numpy(O.rmsnorm(h0.astype(np.float64)).astype(np.float16)).cuda(),
-          torch.empty((T, d), dtype=torch.float16, device="cuda")]
-    idx = torch.empty((T, K), dtype=torch.int32, device="cuda")
-    gw = torch.empty((T, K), dtype=torch.float32, device="cuda")
-    prec = torch.empty((T, K), dtype=torch.int8, device="cuda")
-    seen = {}
-    hmax = 0.0
+    h = torch.from_numpy(C.hidden_states(wl).astype(np.float32)).cuda()
+    # x[l] is layer l's input; the library's own RMSNorm forms x[0]
+    xs = torch.empty((NL + 1, T, d), dtype=torch.float16, device="cuda")
+    S.rmsnorm_device(h, xs[0])
+    idx = torch.empty((NL, T, K), dtype=torch.int32, device="cuda")
+    gw = torch.empty((NL, T, K), dtype=torch.float32, device="cuda")
+    prec = torch.empty((NL, T, K), dtype=torch.int8, device="cuda")
+    h_before, h_after = {}, {}
     for l, L in enumerate(layers):
-        xi, xo = xb[l % 2], xb[(l + 1) % 2]
-        if l in check_layers:
-            torch.cuda.synchronize()
-            before = (xi.cpu().numpy(), h.cpu().numpy())
+        if l in ffn_layers:
+            h_before[l] = h.clone()
         if wl.mode == "prefill":
-            L.prefill_residual(xi, h, xo, idx, gw, prec)
+            L.prefill_residual(xs[l], h, xs[l + 1], idx[l], gw[l], prec[l])
         else:
-            L.decode_step_residual(xi, h, xo, idx, gw, prec)
-        if l in check_layers:
-            torch.cuda.synchronize()
-            seen[l] = before + (h.cpu().numpy(), xo.cpu().numpy(), idx.cpu().numpy(),
-                                gw.cpu().numpy(), prec.cpu().numpy())
+            L.decode_step_residual(xs[l], h, xs[l + 1], idx[l], gw[l], prec[l])
+        if l in ffn_layers:
+            h_after[l] = h.clone()
     torch.cuda.synchronize()
-    hmax = float(h.abs().max().item())
-    finite = bool(torch.isfinite(h).all().item())
+    rec = {"x": xs.cpu().numpy(), "idx": idx.cpu().numpy(), "w": gw.cpu().numpy(),
+           "prec": prec.cpu().numpy(),
+           "h_before": {l: v.cpu().numpy() for l, v in h_before.items()},
+           "h_after": {l: v.cpu().numpy() for l, v in h_after.items()},
+           "hmax": float(h.abs().max().item()), "finite": bool(torch.isfinite(h).all().item())}
     for L in layers:
         L.destroy()
-    del layers, keep, h, xb
+    del layers, keep, h, xs, h_before, h_after
     gc.collect()
     torch.cuda.empty_cache()
-    return seen, hmax, finite
+    return rec
 
 
-def _check_layer(wl, l, rec, rows):
-    x_l, h_l, h_n, x_n, idx, w, prec = rec
+def _check_all_routing(wl, rec):
+    """Routing of every token of every layer against the oracle; returns the
+    oracle routings (near-ties resolved to the device's choice)."""
+    routes, n_flag = [], 0
+    for l in range(wl.n_layers):
+        r, flags = S.check_routing(rec["x"][l], C.router_weight(wl, l), C.layer_tags(wl, l),
+                                   wl.top_k, wl.t1, wl.t2, rec["idx"][l], rec["w"][l],
+                                   rec["prec"][l])
+        routes.append(r)
+        n_flag += len(flags)
+    n = wl.n_layers * wl.n_tokens
+    print(f"{wl.name}: routing exact on {n} routed token-layers "
+          f"({n * wl.top_k} slots), {n_flag} flagged near-ties")
+    return routes
+
+
+def _check_ffn(wl, l, rec, r, rows):
+    x_l = rec["x"][l][rows]
+    h_l, h_n, x_n = rec["h_before"][l][rows], rec["h_after"][l][rows], rec["x"][l + 1][rows]
     tags = C.layer_tags(wl, l)
-    r, flags = S.check_routing(x_l[rows], C.router_weight(wl, l), tags, wl.top_k,
-                               wl.t1, wl.t2, idx[rows], w[rows], prec[rows])
-    y_ref = O.layer_output(x_l[rows], S.HostExperts(wl, l, tags), r)
-    h_ref, x_ref = O.residual_step(h_l[rows].astype(np.float64), y_ref, O.RMS_EPS)
-    inc = h_n[rows].astype(np.float64) - h_l[rows].astype(np.float64)
+    rr = O.Routing(idx=r.idx[rows], w=r.w[rows], prec=r.prec[rows], logits=r.logits[rows])
+    y_ref = O.layer_output(x_l, S.HostExperts(wl, l, tags), rr)
+    h_ref, _ = O.residual_step(h_l.astype(np.float64), y_ref, O.RMS_EPS)
+    inc = h_n.astype(np.float64) - h_l.astype(np.float64)
     e_inc = S.normwise(inc, y_ref).max()
-    e_h = S.normwise(h_n[rows], h_ref).max()
-    e_x = S.normwise(x_n[rows], O.rmsnorm(h_ref)).max()
-    print(f"{wl.name} layer {l}: increment {e_inc:.2e}, h {e_h:.2e}, x_next {e_x:.2e}, "
-          f"flags {len(flags)}")
+    e_h = S.normwise(h_n, h_ref).max()
+    e_x = S.normwise(x_n, O.rmsnorm(h_ref)).max()
+    print(f"{wl.name} layer {l}: increment {e_inc:.2e}, h {e_h:.2e}, x_next {e_x:.2e} "
+          f"on {len(rows)} tokens")
     assert e_inc <= S.TOL and e_h <= S.TOL and e_x <= S.TOL
-    return r
 
 
 def test_phi_stack32_decode_teacher_forced():
     """Phi-MoE-shaped decode stack: 32 layers, 4 tokens per step, per-layer
-    half fp16 / half int4 maps; the multi-token (matrix-core) decode path."""
+    half fp16 / half int4 maps; the multi-token (matrix-core) decode path.
+    Routing on all 128 token-layers; the FFN at 4 layers, every token."""
     wl = C.PHI_STACK
-    check = [0, 1, 15, wl.n_layers - 1]
-    seen, hmax, finite = _run_stack(wl, set(check))
-    print(f"final max|h| {hmax:.3f}")
-    assert finite and hmax < 1e3
-    for l in check:
-        _check_layer(wl, l, seen[l], np.arange(wl.n_tokens))
+    ffn = [0, 1, 15, wl.n_layers - 1]
+    rec = _run_stack(wl, set(ffn))
+    print(f"final max|h| {rec['hmax']:.3f}")
+    assert rec["finite"] and rec["hmax"] < 1e3
+    routes = _check_all_routing(wl, rec)
+    for l in ffn:
+        _check_ffn(wl, l, rec, routes[l], np.arange(wl.n_tokens))
         gc.collect()
 
 
 def test_mixtral_stack32_prefill_teacher_forced():
     """Mixtral-shaped prefill stack: 32 layers of 512 tokens, per-layer
-    4:3:1 maps; 24 sampled tokens at three layers."""
+    4:3:1 maps.  Routing on all 16,384 token-layers; the FFN on 24 sampled
+    tokens at three layers."""
     wl = C.MIXTRAL_PREFILL
-    check = [0, wl.n_layers // 2, wl.n_layers - 1]
-    seen, hmax, finite = _run_stack(wl, set(check))
-    print(f"final max|h| {hmax:.3f}")
-    assert finite and hmax < 1e3
-    rows = np.linspace(0, wl.n_tokens - 1, 24).astype(int)
-    for l in check:
-        r = _check_layer(wl, l, seen[l], rows)
+    ffn = [0, wl.n_layers // 2, wl.n_layers - 1]
+    rec = _run_stack(wl, set(ffn))
+    print(f"final max|h| {rec['hmax']:.3f}")
+    assert rec["finite"] and rec["hmax"] < 1e3
+    routes = _check_all_routing(wl, rec)
+    for r in routes:
         assert np.all(r.prec != O.PREC_SKIP)
+    rows = np.linspace(0, wl.n_tokens - 1, 24).astype(int)
+    for l in ffn:
+        _check_ffn(wl, l, rec, routes[l], rows)
         gc.collect()

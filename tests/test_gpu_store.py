@@ -138,3 +138,28 @@ def test_store_and_bind_errors():
     assert ei.value.status == B.MOE_ESTATE
     L.destroy()
     st.destroy()
+
+
+@pytest.mark.parametrize("bits", [4, 2])
+def test_rebind_rebuilds_quantised_copies(bits):
+    """An expert's library-built low copy is quantised from the fp16 weights
+    it had then; after the expert is bound to other fp16 weights, setting a
+    low-precision tag again must rebuild the copy from the new weights."""
+    wl = _edge(bits)
+    wg, w1, w3, w2 = S.device_layer_weights(wl, 0)
+    import paper_2411_01433_amd as P
+    low = C.TAG_MISS_INT4 if bits == 4 else C.TAG_MISS_INT2
+    L = P.MoeLayer(wl.d_model, wl.d_ff, wl.n_experts, wl.top_k, wl.n_tokens, wg, w1, w3, w2)
+    L.set_expert_precision(0, low)            # copy of expert 0's weights
+    L.bind_expert(0, C.TAG_FP16, w=[w1[1], w3[1], w2[1]])   # expert 0 now holds expert 1's
+    L.set_expert_precision(0, low)            # must quantise expert 1's weights
+    for m, src in enumerate((w1[1], w3[1], w2[1])):
+        rows, cols = src.shape
+        q = torch.empty((rows, cols * bits // 8), dtype=torch.uint8, device="cuda")
+        s = torch.empty((rows, cols // 32), dtype=torch.float16, device="cuda")
+        L.export_packed(0, m, bits, q, s)
+        torch.cuda.synchronize()
+        qr, sr = O.quantize(src.cpu().numpy(), bits)
+        assert np.array_equal(q.cpu().numpy(), O.pack_codes(qr, bits))
+        assert np.array_equal(s.cpu().numpy().view(np.uint16), sr.view(np.uint16))
+    L.destroy()
