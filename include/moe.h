@@ -138,6 +138,27 @@ moe_status moe_decode_step(moe_layer_t layer, int32_t n_tokens, const void* x,
                            float* y, int32_t* topk_idx, float* topk_w,
                            int8_t* prec_used, void* stream);
 
+/* Allocation-free variant of moe_decode_step, for callers that cannot
+ * allocate device memory around a step: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Same kernels and the same
+ * results as moe_decode_step; the call allocates nothing (no hipMalloc, no
+ * hipFree, no allocating library routine).  Its workspace (work list, pair
+ * permutation, routing outputs, SwiGLU activations h and, from 3 tokens on,
+ * the per-pair expert outputs) lives in a static device array of 8 MiB that
+ * each GPU the library runs on holds until the process ends, instead of the
+ * handle's workspace.  A step needs about
+ *   n_tokens * top_k * (2 d_ff + (n_tokens >= 3 ? 4 d_model : 0) + 17) + 2 KiB
+ * bytes of it (each region rounded up to 256 bytes); a larger step returns
+ * MOE_EINVAL with nothing enqueued (a Mixtral-shaped layer, d_model 4096,
+ * d_ff 14336, top-2, fits up to 64 tokens).  Every call on one GPU shares that
+ * GPU's array, which keeps the last call's contents: calls that overlap on one
+ * GPU (other streams, threads or handles) race and must be ordered by the
+ * caller.  Nothing in it needs to start at zero (each call writes what it
+ * reads).  Arguments as moe_decode_step. */
+moe_status moe_decode_step_noalloc(moe_layer_t layer, int32_t n_tokens, const void* x,
+                                   float* y, int32_t* topk_idx, float* topk_w,
+                                   int8_t* prec_used, void* stream);
+
 /* Decode step with the residual glue used between stacked layers:
  *  h       device fp32 [n_tokens, d_model], in/out: h += MoE(x)
  *  x_next  device fp16 [n_tokens, d_model], out: fp16(rmsnorm(h)) with

@@ -30,6 +30,7 @@ EXPORTED = (
     "moe_cache_stats", "moe_cache_destroy",
     "moe_store_create", "moe_store_sizes", "moe_store_put", "moe_store_load",
     "moe_store_destroy", "moe_layer_bind_expert", "moe_rmsnorm",
+    "moe_decode_step_noalloc",
 )
 
 
@@ -78,6 +79,7 @@ def lib() -> ctypes.CDLL:
     L.moe_set_expert_precision.argtypes = [vp, i32, i32, vp]
     step = [vp, i32, vp, f32p, vp, vp, vp, vp]
     L.moe_decode_step.argtypes = step
+    L.moe_decode_step_noalloc.argtypes = step
     L.moe_prefill.argtypes = step
     res = [vp, i32, vp, f32p, vp, vp, vp, vp, vp]
     L.moe_decode_step_residual.argtypes = res
@@ -224,6 +226,11 @@ class MoeLayer:
 
     def decode_step(self, x, y, topk_idx=None, topk_w=None, prec_used=None, stream=None):
         self._step(lib().moe_decode_step, x, y, topk_idx, topk_w, prec_used, stream)
+
+    def decode_step_noalloc(self, x, y, topk_idx=None, topk_w=None, prec_used=None,
+                            stream=None):
+        """moe_decode_step_noalloc: the decode step with the static scratch."""
+        self._step(lib().moe_decode_step_noalloc, x, y, topk_idx, topk_w, prec_used, stream)
 
     def prefill(self, x, y, topk_idx=None, topk_w=None, prec_used=None, stream=None):
         self._step(lib().moe_prefill, x, y, topk_idx, topk_w, prec_used, stream)

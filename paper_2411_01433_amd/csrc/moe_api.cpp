@@ -430,6 +430,10 @@ moe_status moe_layer_init(const moe_layer_desc* desc, const void* w_router,
   l->desc = *desc;
   hipError_t he = hipGetDevice(&l->device);
   if (he != hipSuccess) { delete l; return hip_fail(he, "hipGetDevice"); }
+  // the static scratch of moe_decode_step_noalloc: its address on this
+  // device is looked up here, once per device, with the device current
+  he = scratch_setup(l->device, nullptr);
+  if (he != hipSuccess) { delete l; return hip_fail(he, "scratch address lookup"); }
   l->w_router = static_cast<const f16*>(w_router);
   const int E = desc->n_experts, K = desc->top_k, d = desc->d_model, f = desc->d_ff;
   const int64_t M = desc->max_tokens;
@@ -615,6 +619,49 @@ moe_status moe_decode_step(moe_layer_t l, int32_t n_tokens, const void* x, float
                            void* stream) {
   g_err.clear();
   return decode_impl(l, n_tokens, x, y, nullptr, nullptr, topk_idx, topk_w, prec_used, stream);
+}
+
+moe_status moe_decode_step_noalloc(moe_layer_t l, int32_t T, const void* x, float* y,
+                                   int32_t* topk_idx, float* topk_w, int8_t* prec_used,
+                                   void* stream) {
+  g_err.clear();
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  const int lim = l->desc.max_tokens < kDecodeMaxTokens ? l->desc.max_tokens : kDecodeMaxTokens;
+  moe_status st = check_call(l, T, lim, x, y, nullptr);
+  if (st != MOE_OK) return st;
+  // the layout of the layer's arena, sized for T tokens
+  auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  const size_t P = (size_t)T * l->desc.top_k;
+  size_t off = 0;
+  const size_t o_wl = off;   off += al(sizeof(WorkList));
+  const size_t o_perm = off; off += al(sizeof(int32_t) * P);
+  const size_t o_pos = off;  off += al(sizeof(int32_t) * P);
+  const size_t o_idx = off;  off += al(sizeof(int32_t) * P);
+  const size_t o_w = off;    off += al(sizeof(float) * P);
+  const size_t o_prec = off; off += al(sizeof(int8_t) * P);
+  const size_t o_h = off;    off += al(sizeof(f16) * P * l->desc.d_ff);
+  const size_t o_ep = off;
+  if (T >= kDecodeMfmaMinTokens) off += al(sizeof(float) * P * l->desc.d_model);
+  if (off > scratch_bytes())
+    return fail(MOE_EINVAL,
+                "a %d-token step of this layer needs %zu bytes of scratch; the static scratch "
+                "holds %zu (use fewer tokens per call, or moe_decode_step)",
+                T, off, scratch_bytes());
+  if ((st = set_device(l)) != MOE_OK) return st;
+  void* base_v = nullptr;
+  HIP_TRY(scratch_setup(l->device, &base_v), "scratch address lookup");
+  char* base = static_cast<char*>(base_v);
+  Workspace ws;
+  ws.wl = reinterpret_cast<WorkList*>(base + o_wl);
+  ws.perm = reinterpret_cast<int32_t*>(base + o_perm);
+  ws.pos = reinterpret_cast<int32_t*>(base + o_pos);
+  ws.idx = reinterpret_cast<int32_t*>(base + o_idx);
+  ws.w = reinterpret_cast<float*>(base + o_w);
+  ws.prec = reinterpret_cast<int8_t*>(base + o_prec);
+  ws.h = reinterpret_cast<f16*>(base + o_h);
+  ws.eperm = T >= kDecodeMfmaMinTokens ? reinterpret_cast<float*>(base + o_ep) : nullptr;
+  return decode_launch(l, ws, T, x, y, nullptr, nullptr, topk_idx, topk_w, prec_used,
+                       static_cast<hipStream_t>(stream));
 }
 
 moe_status moe_decode_step_residual(moe_layer_t l, int32_t n_tokens, const void* x,

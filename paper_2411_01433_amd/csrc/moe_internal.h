@@ -105,6 +105,12 @@ struct PredictParams {
   int32_t T, d, E, K, p;
 };
 
+// Static scratch of the allocation-free decode step (noalloc.hip): its size,
+// and its device address on `device` (looked up on the first call, which
+// must find `device` current; later calls return the kept address).
+size_t scratch_bytes();
+hipError_t scratch_setup(int device, void** out);
+
 // ---- launchers (defined in the .hip files) -------------------------------
 hipError_t launch_quantize(const f16* w, int64_t rows, int64_t cols, int bits,
                            uint8_t* codes, f16* scales, hipStream_t s);
