@@ -154,6 +154,17 @@ def step_bytes(wl, idx, prec, tags):
     return total, up
 
 
+def down_bytes(wl, idx, prec, tags):
+    """Algorithmic bytes of one down-projection launch: the W2 part of every
+    distinct copy, the h rows read (fp16) and the expert outputs written
+    (fp32), one per routed (token, slot) pair."""
+    d, f = wl.d_model, wl.d_ff
+    copies = {(int(e), copy_bits(int(tags[int(e)]), int(p)))
+              for e, p in zip(idx.ravel(), prec.ravel()) if p != 2}
+    n_pairs = int((prec != 2).sum())
+    return sum(matrix_bytes(d, f, b) for _, b in copies) + n_pairs * f * 2 + n_pairs * d * 4
+
+
 def cpu_info():
     info = {"cpus_affinity": len(os.sched_getaffinity(0)), "nproc": os.cpu_count()}
     try:
@@ -374,10 +385,12 @@ def run_stack(args):
     idx_h, prec_h = idx.cpu().numpy(), prec.cpu().numpy()
     ups = [step_bytes(wl, idx_h[l], prec_h[l], tags_l[l])[1] for l in range(NL)]
     if args.pmc_pass:
+        downs = [down_bytes(wl, idx_h[l], prec_h[l], tags_l[l]) for l in range(NL)]
         return {"mode": "pmc-pass", "workload": wl.name,
                 "launches": NL * (args.warmup + args.steps),
                 "up_bytes_per_launch_mean": float(np.mean(ups)),
-                "source_sha256": source_sha256(wl.name)}
+                "down_bytes_per_launch_mean": float(np.mean(downs)),
+                "source_sha256": source_sha256(wl.name)}, None
     b, fl = stack_bytes_flops(wl, idx_h, prec_h, tags_l)
     up_flops = [int((prec_h[l] != 2).sum()) * 2 * 2 * d * wl.d_ff for l in range(NL)]
 
