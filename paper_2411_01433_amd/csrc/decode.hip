@@ -59,6 +59,29 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
+// Sum over the 64 lanes of a wave in registers (every lane gets the sum):
+// butterflies inside each 16-lane row by DPP (lane ^ 1, lane ^ 2, mirror
+// in 8, mirror in 16), then the rows pairwise by v_permlane16_swap and the
+// halves by v_permlane32_swap.  __shfl_xor goes through LDS permutes
+// (ds_bpermute), about a hundred cycles per step.
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ inline float wave_sum_dpp(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror
+  v += dpp_f<0x140>(v);  // row_mirror
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = __builtin_bit_cast(float, (uint32_t)r16[0]) + __builtin_bit_cast(float, (uint32_t)r16[1]);
+  const uint32_t w = __builtin_bit_cast(uint32_t, v);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+  return __builtin_bit_cast(float, (uint32_t)r32[0]) + __builtin_bit_cast(float, (uint32_t)r32[1]);
+}
+
 // low half of a | low half of b  /  high half of a | high half of b
 __device__ inline uint32_t lo_lo(uint32_t a, uint32_t b) {
   return __builtin_amdgcn_perm(b, a, 0x05040100u);
@@ -114,18 +137,35 @@ __device__ inline void load_act(const f16* p, uint32_t (&a)[Fmt<BITS>::kEpl / 2]
   }
 }
 
-// One weight piece of one row for one chunk: loaded, then dequantised into
-// the fp16 pairs matching load_act, and its group scale.  Weights are read
+// One weight piece of one row for one chunk: loaded, then multiplied with
+// the activation pairs of load_act, and its group scale.  Weights are read
 // exactly once per step, so they are loaded nontemporally (streaming hint):
 // on MI355X that lifts a pure read stream from ~6.2 to ~6.9 TB/s.
+//
+// Codes become fp16 without shifting each one into place: a code u whose
+// lowest bit sits at bit p of a 16-bit half, or-ed with the exponent of
+// 2^(10-p), is the fp16 number 2^(10-p) + u (one and-or per pair of codes
+// 16 bits apart).  The products then carry the offset o = 2^(10-p) + z of
+// each code (z: the format's zero point, 2^(bits-1)), which is removed once
+// per chunk and token on the activation side:
+//   sum_j (u_j - z) x_j = sum_j (o_j + u_j - z) x_j - sum_j o_j x_j,
+// where the second sum (bias()) depends on the token only and serves every
+// row of the tile.  All products are exact in fp32 (11 x 11 bits); the
+// fp32 sums of the offset products lose about 2^-24 of their magnitude
+// (at most ~1000x the activations) per addition.
 template <int BITS> struct Piece;
+
+__device__ inline uint32_t and_or(uint32_t w, uint32_t mask, uint32_t expo) {
+  return (w & mask) | expo;
+}
 
 template <> struct Piece<16> {
   u32x4 v;
   __device__ inline void load(const ExpertEntry& ex, int m, int64_t row, int64_t ld, int64_t col) {
     v = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.w[m] + row * ld + col)));
   }
-  __device__ inline float dot(const uint32_t (&a)[4], float acc) const {
+  static __device__ inline float bias(const uint32_t (&)[4]) { return 0.0f; }
+  __device__ inline float dot(const uint32_t (&a)[4], float, float acc) const {
     acc = dot2(v.x, a[0], acc);
     acc = dot2(v.y, a[1], acc);
     acc = dot2(v.z, a[2], acc);
@@ -140,20 +180,24 @@ template <> struct Piece<8> {
     v = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(ex.hq[m] + row * ld + col)));
     s = __builtin_nontemporal_load(gmem(ex.hs[m] + row * (ld / kGroup) + col / kGroup));
   }
-  // word holding e0..e3 (e_j in byte j) -> pairs (e0, e2), (e1, e3) - 128
-  static __device__ inline float dot_word(uint32_t w, const uint32_t* a, float g) {
-    const f16x2 bias = as_h2(0x64806480u);  // 1152 = 1024 + 128
-    const f16x2 q0 = as_h2((w & 0x00FF00FFu) | 0x64006400u) - bias;
-    const f16x2 q1 = as_h2(((w >> 8) & 0x00FF00FFu) | 0x64006400u) - bias;
-    g = dot2(__builtin_bit_cast(uint32_t, q0), a[0], g);
-    return dot2(__builtin_bit_cast(uint32_t, q1), a[1], g);
+  // every pair carries 1024 + 128 (p = 0 after the byte shift, z = 128)
+  static __device__ inline float bias(const uint32_t (&a)[8]) {
+    float b = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) b = dot2(a[k], 0x64806480u, b);  // 1152
+    return b;
   }
-  __device__ inline float dot(const uint32_t (&a)[8], float acc) const {
+  // word holding e0..e3 (e_j in byte j) -> pairs (e0, e2), (e1, e3)
+  static __device__ inline float dot_word(uint32_t w, const uint32_t* a, float g) {
+    g = dot2(and_or(w, 0x00FF00FFu, 0x64006400u), a[0], g);
+    return dot2(and_or(w >> 8, 0x00FF00FFu, 0x64006400u), a[1], g);
+  }
+  __device__ inline float dot(const uint32_t (&a)[8], float bias, float acc) const {
     float g = dot_word(v.x, a, 0.0f);
     g = dot_word(v.y, a + 2, g);
     g = dot_word(v.z, a + 4, g);
     g = dot_word(v.w, a + 6, g);
-    return fmaf((float)s, g, acc);
+    return fmaf((float)s, g - bias, acc);
   }
 };
 
@@ -164,20 +208,26 @@ template <> struct Piece<4> {
     v = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x2*>(ex.q[m] + row * (ld / 2) + col / 2)));
     s = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
   }
-  // word holding e0..e7 (e_j at bits 4j) -> pairs (e_k, e_{k+4}) - 8
-  static __device__ inline float dot_word(uint32_t w, const uint32_t* a, float g) {
-    const f16x2 bias = as_h2(0x64086408u);  // 1032 = 1024 + 8
+  // pair k of a word: codes at bits 4k, 16 + 4k; k = 0, 2 sit at p = 0
+  // (offset 1024 + 8), k = 1, 3 at p = 4 (64 + 8), k = 2, 3 after a shift by 8
+  static __device__ inline float bias(const uint32_t (&a)[8]) {
+    float b = 0.0f;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const f16x2 q = as_h2(((w >> (4 * k)) & 0x000F000Fu) | 0x64006400u) - bias;
-      g = dot2(__builtin_bit_cast(uint32_t, q), a[k], g);
-    }
-    return g;
+    for (int k = 0; k < 8; ++k) b = dot2(a[k], (k & 1) ? 0x54805480u : 0x64086408u, b);  // 72 : 1032
+    return b;
   }
-  __device__ inline float dot(const uint32_t (&a)[8], float acc) const {
+  // word holding e0..e7 (e_j at bits 4j) -> pairs (e_k, e_{k+4})
+  static __device__ inline float dot_word(uint32_t w, const uint32_t* a, float g) {
+    const uint32_t w8 = w >> 8;
+    g = dot2(and_or(w, 0x000F000Fu, 0x64006400u), a[0], g);
+    g = dot2(and_or(w, 0x00F000F0u, 0x54005400u), a[1], g);
+    g = dot2(and_or(w8, 0x000F000Fu, 0x64006400u), a[2], g);
+    return dot2(and_or(w8, 0x00F000F0u, 0x54005400u), a[3], g);
+  }
+  __device__ inline float dot(const uint32_t (&a)[8], float bias, float acc) const {
     float g = dot_word(v.x, a, 0.0f);
     g = dot_word(v.y, a + 4, g);
-    return fmaf((float)s, g, acc);
+    return fmaf((float)s, g - bias, acc);
   }
 };
 
@@ -188,16 +238,27 @@ template <> struct Piece<2> {
     v = __builtin_nontemporal_load(gmem(reinterpret_cast<const uint32_t*>(ex.q[m] + row * (ld / 4) + col / 4)));
     s = __builtin_nontemporal_load(gmem(ex.s[m] + row * (ld / kGroup) + col / kGroup));
   }
-  // word holding e0..e15 (e_j at bits 2j) -> pairs (e_k, e_{k+8}) - 2
-  __device__ inline float dot(const uint32_t (&a)[8], float acc) const {
-    const f16x2 bias = as_h2(0x64026402u);  // 1026 = 1024 + 2
+  // pair k: codes at bits 2k, 16 + 2k; k = 0..4 in place (p = 2k), k = 5..7
+  // after a shift by 10 (p = 2k - 10); offsets 2^(10-p) + 2
+  static constexpr uint32_t kMask[8] = {0x00030003u, 0x000C000Cu, 0x00300030u, 0x00C000C0u,
+                                        0x03000300u, 0x00030003u, 0x000C000Cu, 0x00300030u};
+  static constexpr uint32_t kExpo[8] = {0x64006400u, 0x5C005C00u, 0x54005400u, 0x4C004C00u,
+                                        0x44004400u, 0x64006400u, 0x5C005C00u, 0x54005400u};
+  static constexpr uint32_t kOff[8] = {0x64026402u, 0x5C085C08u, 0x54205420u, 0x4C804C80u,  // 1026 258 66 18
+                                       0x46004600u, 0x64026402u, 0x5C085C08u, 0x54205420u}; // 6 1026 258 66
+  static __device__ inline float bias(const uint32_t (&a)[8]) {
+    float b = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) b = dot2(a[k], kOff[k], b);
+    return b;
+  }
+  // word holding e0..e15 (e_j at bits 2j) -> pairs (e_k, e_{k+8})
+  __device__ inline float dot(const uint32_t (&a)[8], float bias, float acc) const {
+    const uint32_t w10 = v >> 10;
     float g = 0.0f;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const f16x2 q = as_h2(((v >> (2 * k)) & 0x00030003u) | 0x64006400u) - bias;
-      g = dot2(__builtin_bit_cast(uint32_t, q), a[k], g);
-    }
-    return fmaf((float)s, g, acc);
+    for (int k = 0; k < 8; ++k) g = dot2(and_or(k < 5 ? v : w10, kMask[k], kExpo[k]), a[k], g);
+    return fmaf((float)s, g - bias, acc);
   }
 };
 
@@ -216,8 +277,11 @@ __device__ inline void tile_dots(const ExpertEntry& ex, const int (&mats)[NM],
     const int64_t col = (int64_t)c * kChunk + lane * kEpl;
     if (col >= ld) continue;  // ragged last chunk (ld is a multiple of 64)
     uint32_t a[NT][kEpl / 2];
+    float bb[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) load_act<BITS>(act_rows[t] + col, a[t]);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) bb[t] = Piece<BITS>::bias(a[t]);
 #pragma unroll
     for (int m = 0; m < NM; ++m) {
       Piece<BITS> pc[ROWS];
@@ -226,7 +290,7 @@ __device__ inline void tile_dots(const ExpertEntry& ex, const int (&mats)[NM],
 #pragma unroll
       for (int i = 0; i < ROWS; ++i)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[m][i][t] = pc[i].dot(a[t], acc[m][i][t]);
+        for (int t = 0; t < NT; ++t) acc[m][i][t] = pc[i].dot(a[t], bb[t], acc[m][i][t]);
     }
   }
 }
@@ -265,12 +329,15 @@ __device__ inline void tile_dots_ring(const ExpertEntry& ex, const int (&mats)[N
   };
   auto dots = [&](int sl, int i) {
     if (col_of(i) < ld) {
+      float bb[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) bb[t] = Piece<BITS>::bias(a[sl][t]);
 #pragma unroll
       for (int m = 0; m < NM; ++m)
 #pragma unroll
         for (int r = 0; r < ROWS; ++r)
 #pragma unroll
-          for (int t = 0; t < NT; ++t) acc[m][r][t] = pc[sl][m][r].dot(a[sl][t], acc[m][r][t]);
+          for (int t = 0; t < NT; ++t) acc[m][r][t] = pc[sl][m][r].dot(a[sl][t], bb[t], acc[m][r][t]);
     }
   };
   load(0, 0);
@@ -298,7 +365,7 @@ __device__ inline void block_reduce(float (&acc)[NM][ROWS][NT], float* red) {
     for (int i = 0; i < ROWS; ++i)
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const float s = wave_sum(acc[m][i][t]);
+        const float s = wave_sum_dpp(acc[m][i][t]);
         if (lane == 0) red[wave * V + (m * ROWS + i) * NT + t] = s;
       }
   __syncthreads();
