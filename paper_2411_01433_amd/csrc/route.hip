@@ -29,10 +29,26 @@ __device__ inline float dot2(uint32_t a, uint32_t b, float acc) {
                                 __builtin_bit_cast(f16x2, b), acc, false);
 }
 
+// Sum over the 64 lanes of a wave in registers (every lane gets the sum):
+// DPP butterflies inside each 16-lane row, then v_permlane16_swap and
+// v_permlane32_swap across rows.  The decode and prefill routers both sum
+// their logits with it, so their logits stay bit-identical.
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
 __device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror
+  v += dpp_f<0x140>(v);  // row_mirror
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = __builtin_bit_cast(float, (uint32_t)r16[0]) + __builtin_bit_cast(float, (uint32_t)r16[1]);
+  const uint32_t w = __builtin_bit_cast(uint32_t, v);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+  return __builtin_bit_cast(float, (uint32_t)r32[0]) + __builtin_bit_cast(float, (uint32_t)r32[1]);
 }
 
 // Dot products of tokens [t0, t1) against all E gate rows.  One wave per
