@@ -349,6 +349,8 @@ def run_stack(args):
         keep.append(w)
         tags_l.append(tags)
         layers.append(S.make_layer(wl, tags, w, max_tokens=T))
+        if l > 0:  # the layers run in turn: one workspace serves them all
+            layers[l].share_workspace(layers[0])
     h0 = torch.from_numpy(C.hidden_states(wl).astype(np.float32)).to(dev)
     h = torch.empty_like(h0)
     # the first layer's input, by the library's own RMSNorm of the glue

@@ -42,7 +42,8 @@
  *    failure on the calling thread.
  *  - No C++ exception crosses this interface.
  *  - One handle must not be used from two streams concurrently (it owns a
- *    single workspace).
+ *    single workspace, which moe_layer_share_workspace may share with
+ *    other handles).
  */
 #ifndef MOE_H
 #define MOE_H
@@ -218,8 +219,32 @@ moe_status moe_layer_enable_timing(moe_layer_t layer, int32_t enable);
 moe_status moe_layer_stage_times(moe_layer_t layer, double* ms,
                                  int32_t* n_calls);
 
+/* Run `layer` on the per-call workspace of `owner` and free its own.  The
+ * workspace (work list, pair permutation and positions, routing buffers,
+ * h [max_tokens*top_k, d_ff] fp16 and the per-pair outputs [max_tokens*top_k,
+ * d_model] fp32) holds nothing between calls, so the layers of a stack
+ * (Eq. 1 applied layer after layer), which run one after another, can all
+ * use one: about 46 MB per Mixtral-shaped layer at 512 prefill tokens.
+ * The layer keeps its own expert table, copies and tags.
+ *  - Both must have equal d_model, d_ff, top_k and max_tokens and live on
+ *    the same device (else MOE_EINVAL).  If `owner` itself runs on another
+ *    layer's workspace, `layer` joins that one.
+ *  - Calls on layers that share a workspace must not overlap: enqueue them
+ *    on one stream, or order the streams.  moe_decode_step_noalloc is not
+ *    affected (it uses the static scratch).
+ *  - Sharing twice with the same workspace is a no-op.  A layer that
+ *    already runs on another workspace, or whose workspace others share,
+ *    cannot be re-shared (MOE_ESTATE).
+ *  - The workspace's owner must be destroyed last: moe_layer_destroy on it
+ *    fails with MOE_ESTATE while other layers share it.
+ * Synchronises the device (the freed workspace may be in use by earlier
+ * work); `stream` orders the copy of the expert table to its new place. */
+moe_status moe_layer_share_workspace(moe_layer_t layer, moe_layer_t owner, void* stream);
+
 /* Free the handle, its workspace and its low-precision copies (synchronises
- * the device first).  The borrowed fp16 weights are not touched. */
+ * the device first).  The borrowed fp16 weights are not touched.  Fails
+ * with MOE_ESTATE, freeing nothing, while other layers run on its
+ * workspace (moe_layer_share_workspace). */
 moe_status moe_layer_destroy(moe_layer_t layer);
 
 /* ---- Expert storage and loading (Dynamic Expert Loader) ---------------

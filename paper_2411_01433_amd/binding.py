@@ -22,7 +22,8 @@ EXPORTED = (
     "moe_layer_init", "moe_set_expert_precision", "moe_decode_step",
     "moe_decode_step_residual", "moe_prefill", "moe_prefill_residual",
     "moe_export_packed", "moe_quantize", "moe_layer_enable_timing",
-    "moe_layer_stage_times", "moe_layer_destroy", "moe_last_error",
+    "moe_layer_stage_times", "moe_layer_destroy", "moe_layer_share_workspace",
+    "moe_last_error",
     "moe_predictor_init", "moe_predict", "moe_predictor_destroy",
     "moe_cache_create", "moe_cache_begin_sequence", "moe_cache_begin_token",
     "moe_cache_access", "moe_cache_contains", "moe_cache_set_mask",
@@ -90,6 +91,7 @@ def lib() -> ctypes.CDLL:
     L.moe_layer_stage_times.argtypes = [vp, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int32)]
     L.moe_layer_destroy.argtypes = [vp]
+    L.moe_layer_share_workspace.argtypes = [vp, vp, vp]
     pi32 = ctypes.POINTER(ctypes.c_int32)
     L.moe_cache_create.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(vp)]
     L.moe_cache_begin_sequence.argtypes = [vp]
@@ -288,11 +290,19 @@ class MoeLayer:
         _check(lib().moe_layer_stage_times(self._h, ms, ctypes.byref(n)))
         return list(ms), n.value
 
+    def share_workspace(self, owner: "MoeLayer", stream=None):
+        """Run this layer on owner's per-call workspace and free its own (the
+        layers of a stack run one after another).  Equal d, f, top_k and
+        max_tokens; owner is kept alive by this layer."""
+        _check(lib().moe_layer_share_workspace(self._h, owner._h, _stream(stream)))
+        self._ws_owner = owner
+
     def destroy(self):
         if self._h is not None and self._h.value:
             _check(lib().moe_layer_destroy(self._h))
         self._h = None
         self._keep = None
+        self._ws_owner = None
 
     def __del__(self):
         try:

@@ -76,7 +76,11 @@ struct moe_layer {
   // device memory
   ExpertEntry* d_table = nullptr;
   Workspace ws;             // carved from the arena, sized for max_tokens
-  void* arena = nullptr;
+  void* arena = nullptr;    // the table and, unless shared, the workspace
+  // workspace sharing (stacks): the layer whose workspace this one runs on,
+  // and how many layers run on this one's
+  moe_layer* ws_owner = nullptr;
+  int ws_sharers = 0;
   // stage timing (measurement only): 5 events per recorded call
   bool timing = false;
   std::vector<hipEvent_t> ev_pool;
@@ -770,12 +774,62 @@ moe_status moe_layer_stage_times(moe_layer_t l, double* ms, int32_t* n_calls) {
   return MOE_OK;
 }
 
+moe_status moe_layer_share_workspace(moe_layer_t l, moe_layer_t owner, void* stream) {
+  g_err.clear();
+  if (!l || !owner) return fail(MOE_EINVAL, "layer and owner must be non-NULL");
+  if (l == owner) return fail(MOE_EINVAL, "a layer cannot share its own workspace");
+  moe_layer* o = nullptr;
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    if (!g_live.count(l) || !g_live.count(owner))
+      return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+    o = owner->ws_owner ? owner->ws_owner : owner;  // the workspace's owner
+    if (l->ws_owner == o) return MOE_OK;             // already shared
+    if (l->ws_owner) return fail(MOE_ESTATE, "the layer already runs on another layer's workspace");
+    if (l->ws_sharers > 0)
+      return fail(MOE_ESTATE, "%d layer(s) run on this layer's workspace", l->ws_sharers);
+  }
+  const moe_layer_desc &a = l->desc, &b = o->desc;
+  if (a.d_model != b.d_model || a.d_ff != b.d_ff || a.top_k != b.top_k ||
+      a.max_tokens != b.max_tokens)
+    return fail(MOE_EINVAL, "shared workspaces need equal d_model, d_ff, top_k and max_tokens");
+  if (l->device != o->device) return fail(MOE_EINVAL, "the layers live on different devices");
+  moe_status st = set_device(l);
+  if (st != MOE_OK) return st;
+  // a table-only arena replaces the layer's own (table + workspace)
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t tb = sizeof(ExpertEntry) * a.n_experts;
+  void* t = nullptr;
+  hipError_t he = hipMalloc(&t, tb);
+  if (he != hipSuccess) return fail(MOE_ENOMEM, "hipMalloc of %zu table bytes failed", tb);
+  he = hipMemcpyAsync(t, l->d_table, tb, hipMemcpyDeviceToDevice, s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
+  if (he == hipSuccess) he = hipDeviceSynchronize();  // nothing may still use the old arena
+  if (he != hipSuccess) {
+    (void)hipFree(t);
+    return hip_fail(he, "share workspace copy");
+  }
+  (void)hipFree(l->arena);
+  l->arena = t;
+  l->d_table = static_cast<ExpertEntry*>(t);
+  l->ws = o->ws;
+  std::lock_guard<std::mutex> g(g_mu);
+  l->ws_owner = o;
+  ++o->ws_sharers;
+  return MOE_OK;
+}
+
 moe_status moe_layer_destroy(moe_layer_t l) {
   g_err.clear();
   if (!l) return fail(MOE_EINVAL, "layer is NULL");
   {
     std::lock_guard<std::mutex> g(g_mu);
-    if (!g_live.erase(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+    if (!g_live.count(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+    if (l->ws_sharers > 0)
+      return fail(MOE_ESTATE, "%d layer(s) still run on this layer's workspace; destroy them first",
+                  l->ws_sharers);
+    g_live.erase(l);
+    if (l->ws_owner) --l->ws_owner->ws_sharers;
   }
   hipError_t he = hipSetDevice(l->device);
   if (he == hipSuccess) he = hipDeviceSynchronize();

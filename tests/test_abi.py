@@ -98,6 +98,9 @@ def test_calls_on_invalid_handles_fail_cleanly():
     assert L.moe_export_packed(bogus, 0, 0, 4, x, x, None) == B.MOE_ESTATE
     assert L.moe_layer_destroy(bogus) == B.MOE_ESTATE
     assert L.moe_layer_destroy(None) == B.MOE_EINVAL
+    assert L.moe_layer_share_workspace(bogus, ctypes.c_void_p(0xbeef0), None) == B.MOE_ESTATE
+    assert L.moe_layer_share_workspace(bogus, bogus, None) == B.MOE_EINVAL
+    assert L.moe_layer_share_workspace(None, bogus, None) == B.MOE_EINVAL
     assert b"handle" in L.moe_last_error() or b"NULL" in L.moe_last_error()
 
 
