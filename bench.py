@@ -57,7 +57,7 @@ CSRC = os.path.join(ROOT, "paper_2411_01433_amd", "csrc")
 PMC_SUMMARIES = {
     "mixtral_layer_decode_t1": ("decode_up_mixtral_t1_pmc.md", "decode.hip"),
     "mixtral_layer_decode_t8_skew": ("decode_up_mfma_mixtral_t8_skew_pmc.md", "decode_mfma.hip"),
-    "phi_moe_stack32_decode_t4": ("decode_up_mfma_phi_stack32_t4_pmc.md", "decode_mfma.hip"),
+    "phi_moe_stack32_decode_t4": ("decode_up_phi_stack32_t4_pmc.md", "decode.hip"),
     "mixtral_stack32_prefill_t512": ("prefill_up_mixtral_stack32_t512_pmc.md", "prefill.hip"),
 }
 # arithmetic type of the path: fp16 activations and dequantised weights into
@@ -134,6 +134,15 @@ def copy_bits(tag, prec):
     if prec == 0:
         return 8 if tag in (5, 6) else 16
     return 4 if tag in (1, 3) else 2
+
+
+def decode_up_kernel_name(T, K, E):
+    """The up-projection kernel the library runs for a decode step: the dot2
+    kernel for 1-2 tokens, and up to 8 while T * K <= E; else the
+    matrix-core kernel."""
+    if T <= 2 or (T <= 8 and T * K <= E):
+        return "decode_up_kernel"
+    return "decode_up_mfma_kernel"
 
 
 def step_bytes(wl, idx, prec, tags):
@@ -307,7 +316,7 @@ def run_decode_layer(args):
         "event_overhead_us": event_us,
         "roofline": {"bound": "hbm",
                      # the library takes the matrix-core kernels from 3 tokens per step
-                     "kernel": "decode_up_kernel" if T < 3 else "decode_up_mfma_kernel",
+                     "kernel": decode_up_kernel_name(T, wl.top_k, wl.n_experts),
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
                      "traffic_source": traffic_note,
@@ -443,7 +452,7 @@ def run_stack(args):
     t_s = ms * 1e-3
     frac = max(b / 8e12, fl / 2.5e15) / t_s
     kernel = "prefill_up_kernel" if prefill else (
-        "decode_up_mfma_kernel" if T >= 3 else "decode_up_kernel")
+        decode_up_kernel_name(T, K, wl.n_experts))
     out = {
         "metric": METRIC, "value": T / t_s, "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,

@@ -538,8 +538,10 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
     x_next[base + c] = (f16)(h_res[base + c] * r);
 }
 
-// The host takes these kernels for one or two tokens per step; from three
-// tokens the matrix-core kernels run instead.
+// The host takes these kernels for one or two tokens per step, and for up
+// to kDecodeDot2MaxTokens while the step's pairs do not outnumber the
+// experts; tiles hold one or two tokens (a group of more streams its rows
+// once per tile).
 int nt_max(int T) { return T <= 1 ? 1 : 2; }
 
 }  // namespace
@@ -547,7 +549,7 @@ int nt_max(int T) { return T <= 1 ? 1 : 2; }
 hipError_t launch_decode_up(const ExpertEntry* table, const WorkList* wl,
                             const int32_t* perm, const f16* x, f16* h, int T,
                             int d, int f, int K, int max_groups, hipStream_t s) {
-  if (T < 1 || T > 2) return hipErrorInvalidValue;
+  if (T < 1 || T > kDecodeDot2MaxTokens) return hipErrorInvalidValue;
   dim3 grid(f / UpRows<2>::value, max_groups);
   if (nt_max(T) == 1) decode_up_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K);
   else decode_up_kernel<2><<<grid, kThreads, 0, s>>>(table, wl, perm, x, h, d, f, K);
@@ -558,7 +560,7 @@ hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
                               const int32_t* perm, const float* gate_w,
                               const f16* h, float* y, float* h_res, int T, int d,
                               int f, int K, hipStream_t s) {
-  if (T < 1 || T > 2) return hipErrorInvalidValue;
+  if (T < 1 || T > kDecodeDot2MaxTokens) return hipErrorInvalidValue;
   dim3 grid(d / DownRows<2>::value);
   if (nt_max(T) == 1)
     decode_down_kernel<1><<<grid, kThreads, 0, s>>>(table, wl, perm, gate_w, h, y, h_res, T, d, f, K);

@@ -178,7 +178,15 @@ hipError_t mark(moe_layer* l, int slot, hipStream_t s) {
   return hipEventRecord(l->ev_pool[at], s);
 }
 
-constexpr int kDecodeMfmaMinTokens = 3;
+// Which decode kernels a step takes.  The dot2 kernels stream each expert
+// copy once per two tokens of its group, the matrix-core kernels once per
+// 16; with at most about one token per expert copy (T*K <= E) the dot2
+// kernels' smaller blocks win (Phi-shaped layer, 4 tokens: 148 -> 134 us per
+// step), with more they lose (Mixtral-shaped, 8 tokens: 313 -> 393 us).
+bool decode_on_matrix_cores(int T, int K, int E) {
+  if (T <= 2) return false;
+  return T > kDecodeDot2MaxTokens || T * K > E;
+}
 
 // The launch sequence of a decode step with the workspace `ws` (the layer's
 // arena, or the static scratch of the allocation-free entry point).
@@ -191,9 +199,9 @@ moe_status decode_launch(moe_layer* l, const Workspace& ws, int32_t T, const voi
   HIP_TRY(launch_route_decode(route_params(l, T, x), route_out(ws, idx, w, prec),
                               ws.wl, ws.perm, ws.pos, s), "route kernel launch");
   HIP_TRY(mark(l, 1, s), "timing event");
-  if (T >= kDecodeMfmaMinTokens) {
-    // several tokens per step: matrix-core kernels, per-pair down rows and
-    // the fused combine (+ residual rmsnorm) of the prefill path
+  if (decode_on_matrix_cores(T, K, l->desc.n_experts)) {
+    // several tokens per expert copy: matrix-core kernels, per-pair down
+    // rows and the fused combine (+ residual rmsnorm) of the prefill path
     HIP_TRY(launch_decode_up_mfma(l->d_table, ws.wl, ws.perm, static_cast<const f16*>(x),
                                   ws.h, d, f, K, mg, s), "up kernel launch");
     HIP_TRY(mark(l, 2, s), "timing event");
@@ -645,7 +653,8 @@ moe_status moe_decode_step_noalloc(moe_layer_t l, int32_t T, const void* x, floa
   const size_t o_prec = off; off += al(sizeof(int8_t) * P);
   const size_t o_h = off;    off += al(sizeof(f16) * P * l->desc.d_ff);
   const size_t o_ep = off;
-  if (T >= kDecodeMfmaMinTokens) off += al(sizeof(float) * P * l->desc.d_model);
+  const bool mc = decode_on_matrix_cores(T, l->desc.top_k, l->desc.n_experts);
+  if (mc) off += al(sizeof(float) * P * l->desc.d_model);
   if (off > scratch_bytes())
     return fail(MOE_EINVAL,
                 "a %d-token step of this layer needs %zu bytes of scratch; the static scratch "
@@ -663,7 +672,7 @@ moe_status moe_decode_step_noalloc(moe_layer_t l, int32_t T, const void* x, floa
   ws.w = reinterpret_cast<float*>(base + o_w);
   ws.prec = reinterpret_cast<int8_t*>(base + o_prec);
   ws.h = reinterpret_cast<f16*>(base + o_h);
-  ws.eperm = T >= kDecodeMfmaMinTokens ? reinterpret_cast<float*>(base + o_ep) : nullptr;
+  ws.eperm = mc ? reinterpret_cast<float*>(base + o_ep) : nullptr;
   return decode_launch(l, ws, T, x, y, nullptr, nullptr, topk_idx, topk_w, prec_used,
                        static_cast<hipStream_t>(stream));
 }

@@ -21,6 +21,7 @@ constexpr int kMaxExperts = 64;
 constexpr int kMaxTopK = 8;
 constexpr int kMaxKeys = 2 * kMaxExperts;  // (expert, high|low) work groups
 constexpr int kDecodeMaxTokens = 64;
+constexpr int kDecodeDot2MaxTokens = 8;  // most tokens per step the dot2 decode kernels take
 
 enum { PREC_HIGH = 0, PREC_LOW = 1, PREC_SKIP = 2 };
 enum { TAG_FP16 = 0, TAG_INT4 = 1, TAG_INT2 = 2, TAG_MISS_INT4 = 3,

@@ -62,8 +62,9 @@ def _stack(T, prefill):
     return wl, layers, keep, step, snapshot
 
 
-@pytest.mark.parametrize("T,prefill", [(1, False), (4, False), (37, True)],
-                         ids=["decode_t1", "decode_t4_matrix_core", "prefill_t37"])
+@pytest.mark.parametrize("T,prefill", [(1, False), (4, False), (9, False), (37, True)],
+                         ids=["decode_t1", "decode_t4_dot2", "decode_t9_matrix_core",
+                              "prefill_t37"])
 def test_graph_replay_matches_eager(T, prefill):
     wl, layers, keep, step, snapshot = _stack(T, prefill)
     step()

@@ -225,14 +225,29 @@ def test_many_tokens_per_expert():
 
 @pytest.mark.parametrize("T", [1, 2, 3, 4, 9, 16, 17])
 def test_token_counts_both_decode_kernels(T):
-    """Steps of one or two tokens take the dot2 kernels, larger steps the
-    matrix-core kernels; every tag kind, ragged d and f, groups of more than
-    16 tokens at T = 17 (K = E)."""
+    """Steps of one or two tokens take the dot2 kernels; here K = E, so every
+    larger step has more pairs than experts and takes the matrix-core
+    kernels; every tag kind, ragged d and f, groups of more than 16 tokens
+    at T = 17."""
     wl = _edge("edge_tokens", 36, 320, 448, 5, 5, T,
                [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4, C.TAG_MISS_INT2],
                t1=0.3, t2=0.8)
     rng = np.random.default_rng(100 + T)
     _layer_case(wl, wl.fixed_tags, rng.standard_normal((T, 320)).astype(np.float16))
+
+
+@pytest.mark.parametrize("T", [3, 5, 8])
+def test_multi_token_steps_on_dot2_kernels(T):
+    """Steps of 3 to 8 tokens whose pairs do not outnumber the experts
+    (T * K <= E) take the dot2 kernels, in tiles of two tokens (groups of
+    up to T tokens); every tag kind, ragged d and f."""
+    wl = _edge("edge_dot2_multi", 38, 320, 448, 16, 2, T,
+               [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4] * 4,
+               t1=0.3, t2=0.8)
+    rng = np.random.default_rng(200 + T)
+    _layer_case(wl, wl.fixed_tags, rng.standard_normal((T, 320)).astype(np.float16))
+    _layer_case(wl, wl.fixed_tags, rng.standard_normal((T, 320)).astype(np.float16),
+                residual=True)
 
 
 def test_reduction_chunks():

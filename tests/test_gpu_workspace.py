@@ -47,8 +47,9 @@ def _run(layers, wl, prefill):
     return [t.cpu().numpy() for t in (h, xb[NL % 2], idx, gw, prec)]
 
 
-@pytest.mark.parametrize("T,prefill", [(1, False), (4, False), (37, True)],
-                         ids=["decode_t1", "decode_t4_matrix_core", "prefill_t37"])
+@pytest.mark.parametrize("T,prefill", [(1, False), (4, False), (9, False), (37, True)],
+                         ids=["decode_t1", "decode_t4_dot2", "decode_t9_matrix_core",
+                              "prefill_t37"])
 def test_shared_workspace_matches_own(T, prefill):
     wl = _workload(T)
     keep, layers = [], []
