@@ -56,6 +56,7 @@ CSRC = os.path.join(ROOT, "paper_2411_01433_amd", "csrc")
 # while that source is unchanged.
 PMC_SUMMARIES = {
     "mixtral_layer_decode_t1": ("decode_up_mixtral_t1_pmc.md", "decode.hip"),
+    "mixtral_int8_layer_decode_t1": ("decode_up_mixtral_int8_t1_pmc.md", "decode.hip"),
     "mixtral_layer_decode_t8_skew": ("decode_up_mfma_mixtral_t8_skew_pmc.md", "decode_mfma.hip"),
     "phi_moe_stack32_decode_t4": ("decode_up_phi_stack32_t4_pmc.md", "decode.hip"),
     "mixtral_stack32_prefill_t512": ("prefill_up_mixtral_stack32_t512_pmc.md", "prefill.hip"),
