@@ -518,24 +518,48 @@ __global__ __launch_bounds__(kThreads) void decode_down_kernel(
 }
 
 // ------------------------------------------------------ residual RMSNorm
-__global__ __launch_bounds__(kThreads) void rmsnorm_kernel(
+// One block of 1024 threads per token.  Each thread keeps its float4
+// pieces of the row in registers (d <= 16384: at most 4 per thread), so
+// h_res is read once; sum of squares per thread, over the wave in
+// registers, then over the 16 waves in a fixed order.
+constexpr int kNormThreads = 1024;
+constexpr int kNormPieces = 4;  // float4 pieces per thread: 16384 / (1024 * 4)
+
+__global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
     const float* __restrict__ h_res, f16* __restrict__ x_next, int d, float eps) {
-  __shared__ float red[kWaves];
+  __shared__ float red[kNormThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * d;
+  const f32x4* src = reinterpret_cast<const f32x4*>(h_res + base);
+  const int n4 = d >> 2;  // d is a multiple of 64
+  f32x4 v[kNormPieces];
   float ss = 0.0f;
-  for (int c = threadIdx.x; c < d; c += kThreads) {
-    const float v = h_res[base + c];
-    ss = fmaf(v, v, ss);
+#pragma unroll
+  for (int i = 0; i < kNormPieces; ++i) {
+    const int q = threadIdx.x + i * kNormThreads;
+    v[i] = q < n4 ? src[q] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    ss = fmaf(v[i].x, v[i].x, ss);
+    ss = fmaf(v[i].y, v[i].y, ss);
+    ss = fmaf(v[i].z, v[i].z, ss);
+    ss = fmaf(v[i].w, v[i].w, ss);
   }
-  ss = wave_sum(ss);
+  ss = wave_sum_dpp(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
   float tot = 0.0f;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) tot += red[w];
+  for (int w = 0; w < kNormThreads / 64; ++w) tot += red[w];
   const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += kThreads)
-    x_next[base + c] = (f16)(h_res[base + c] * r);
+  f16* dst = x_next + base;
+#pragma unroll
+  for (int i = 0; i < kNormPieces; ++i) {
+    const int q = threadIdx.x + i * kNormThreads;
+    if (q < n4) {
+      const f16x2 lo = {(f16)(v[i].x * r), (f16)(v[i].y * r)};
+      const f16x2 hi = {(f16)(v[i].z * r), (f16)(v[i].w * r)};
+      *reinterpret_cast<u32x2*>(dst + 4 * q) =
+          u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+    }
+  }
 }
 
 // The host takes these kernels for one or two tokens per step, and for up
@@ -571,7 +595,7 @@ hipError_t launch_decode_down(const ExpertEntry* table, const WorkList* wl,
 
 hipError_t launch_rmsnorm(const float* h_res, f16* x_next, int T, int d,
                           float eps, hipStream_t s) {
-  rmsnorm_kernel<<<T, kThreads, 0, s>>>(h_res, x_next, d, eps);
+  rmsnorm_kernel<<<T, kNormThreads, 0, s>>>(h_res, x_next, d, eps);
   return hipGetLastError();
 }
 
