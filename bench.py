@@ -316,7 +316,6 @@ def run_decode_layer(args):
         "stage_us": dict(zip(["route", "up", "down_combine", "empty"], stage_us)),
         "event_overhead_us": event_us,
         "roofline": {"bound": "hbm",
-                     # the library takes the matrix-core kernels from 3 tokens per step
                      "kernel": decode_up_kernel_name(T, wl.top_k, wl.n_experts),
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
@@ -430,6 +429,16 @@ def run_stack(args):
     b, fl = stack_bytes_flops(wl, idx_h, prec_h, tags_l)
     up_flops = [int((prec_h[l] != 2).sum()) * 2 * 2 * d * wl.d_ff for l in range(NL)]
 
+    # per-pass distribution: one event between consecutive passes
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record()
+    for j in range(args.steps):
+        run()
+        evs[j + 1].record()
+    torch.cuda.synchronize()
+    per_pass = np.array([evs[j].elapsed_time(evs[j + 1]) for j in range(args.steps)])
+    p10, p50, p90 = (float(v) for v in np.percentile(per_pass, [10, 50, 90]))
+
     log("stage timing pass")
     for L in layers:
         L.enable_timing(True)
@@ -469,6 +478,7 @@ def run_stack(args):
         "mfma_util_step": fl / t_s / 2.5e15 if prefill else None,
         "roofline_step": {"bound": "hbm" if b / 8e12 >= fl / 2.5e15 else "mfma",
                           "frac": frac},
+        "pass_ms_p10_p50_p90": [p10, p50, p90],
         "stage_us_per_layer": dict(zip(["route", "up", "down", "glue"], stage_us)),
         "event_overhead_us": ev_us,
         "roofline": {"bound": "hbm", "kernel": kernel,
