@@ -87,6 +87,7 @@ template <int BITS> struct WSrc {
   const f16* srow;       // scales of row n, from this lane group's first group
   int chunk;             // chunk index of the load lane (l / 8)
   int ngr;               // groups per row
+  const uint8_t* dummy;  // target of ring loads past the last stage: this lane's activations
 };
 
 template <int BITS>
@@ -100,6 +101,7 @@ __device__ inline WSrc<BITS> wsrc(const ExpertEntry& ex, int m, int64_t row0, in
   s.row = base + (row0 + (l & 7)) * rb + 16 * s.chunk;
   s.row8 = 8 * rb;
   s.ngr = (int)(ld / kGroup);
+  s.dummy = nullptr;
   s.srow = BITS == 16 ? nullptr
                       : (BITS == 8 ? ex.hs[m] : ex.s[m]) + (row0 + (l & 15)) * s.ngr +
                             Geo<BITS>::kScales * (l >> 4);
@@ -109,7 +111,9 @@ __device__ inline WSrc<BITS> wsrc(const ExpertEntry& ex, int m, int64_t row0, in
 // Load stage kk (first column, a multiple of the stage width).  Chunks past
 // the row end (the last stage of a code row may be partial) read the row's
 // first chunk instead and get scale 0 at use; scales are read in aligned
-// group pairs clamped to the row.  Nothing outside the row is touched.
+// group pairs clamped to the row.  Nothing outside the row is touched,
+// except by a ring slot past the wave's last stage (kk < 0), which reads
+// 32 bytes of the lane's activation row (s.dummy) instead.
 template <int BITS>
 __device__ inline void load_w(const WSrc<BITS>& s, int64_t kk, int64_t ld, WStage<BITS>& w) {
   using G = const __attribute__((address_space(1))) u32x4*;
@@ -118,9 +122,14 @@ __device__ inline void load_w(const WSrc<BITS>& s, int64_t kk, int64_t ld, WStag
     const bool ok = kk + (int64_t)(s.chunk + 1) * Geo<BITS>::kChunkCols <= ld;
     off = ok ? off : -16 * (int64_t)s.chunk;
   }
-  const uint8_t* p = s.row + off;
+  // kk < 0: a ring slot past the wave's last stage; its data is never
+  // used, so the loads read this lane's activation row, which L2 holds
+  // (reloading the wave's last stage re-read it from HBM: the streaming
+  // loads do not keep it; one shared line would be a hot spot)
+  const bool past = kk < 0;
+  const uint8_t* p = past ? s.dummy : s.row + off;
   w.v[0] = __builtin_nontemporal_load(reinterpret_cast<G>(gmem(p)));
-  w.v[1] = __builtin_nontemporal_load(reinterpret_cast<G>(gmem(p + s.row8)));
+  w.v[1] = __builtin_nontemporal_load(reinterpret_cast<G>(gmem(past ? p : p + s.row8)));
   if (BITS != 16) {
     using S = const __attribute__((address_space(1))) uint32_t*;
     const int g = (threadIdx.x & 63) >> 4;
@@ -130,7 +139,8 @@ __device__ inline void load_w(const WSrc<BITS>& s, int64_t kk, int64_t ld, WStag
       // int8: one group per lane, read with its even neighbour
       const int idx = min(BITS == 8 ? (gi & ~1) : gi + 2 * h, s.ngr - 2);
       w.s[h] = __builtin_nontemporal_load(
-          reinterpret_cast<S>(gmem(s.srow - Geo<BITS>::kScales * g + idx)));
+          reinterpret_cast<S>(gmem(past ? reinterpret_cast<const f16*>(s.dummy)
+                                        : s.srow - Geo<BITS>::kScales * g + idx)));
     }
   }
 }
@@ -351,15 +361,19 @@ __device__ inline void tile_gemm(const ExpertEntry& ex, const int (&mats)[NM], i
   if (nst <= 0) return;
   WSrc<BITS> src[NM];
 #pragma unroll
-  for (int m = 0; m < NM; ++m) src[m] = wsrc<BITS>(ex, mats[m], row0, ld);
+  for (int m = 0; m < NM; ++m) {
+    src[m] = wsrc<BITS>(ex, mats[m], row0, ld);
+    src[m].dummy = reinterpret_cast<const uint8_t*>(arow);
+  }
   auto col = [&](int64_t i) { return (wave + (i < nst ? i : nst - 1) * kWaves) * (int64_t)GG::kCols; };
+  auto wcol = [&](int64_t i) { return i < nst ? col(i) : (int64_t)-1; };  // -1: past the end
   WStage<BITS> w[D][NM];
   AStage<BITS> a[D];
 #pragma unroll
   for (int u = 0; u < D; ++u) {
     const int64_t kk = col(u);
 #pragma unroll
-    for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
+    for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], wcol(u), ld, w[u][m]);
     load_a<BITS>(arow, kk, ld, a[u]);
   }
   int64_t i0 = 0;
@@ -369,7 +383,7 @@ __device__ inline void tile_gemm(const ExpertEntry& ex, const int (&mats)[NM], i
       consume<BITS, NM>(w[u], a[u], col(i0 + u), ld, acc);
       const int64_t kk = col(i0 + u + D);
 #pragma unroll
-      for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], kk, ld, w[u][m]);
+      for (int m = 0; m < NM; ++m) load_w<BITS>(src[m], wcol(i0 + u + D), ld, w[u][m]);
       load_a<BITS>(arow, kk, ld, a[u]);
       // keep the ring order: the scheduler would otherwise sink the loads
       // below the products and wait for nearly all of them each round

@@ -348,10 +348,11 @@ __device__ void gemm_pass(const ExpertEntry& ex, int64_t wrow0, int64_t ld,
     src[rt][0] = wrow<BITS, M0>(ex, row, ld);
     if constexpr (NM == 2) src[rt][1] = wrow<BITS, M0 + 1>(ex, row, ld);
   }
-  // stages past the end reload stage 0 (never multiplied): unconditional
-  // loads, see ActStager
+  // ring slots past the last stage (never multiplied) reload the last
+  // stage, which the ring loaded a few stages before and L2 still holds
+  // (stage 0 would come from HBM again): unconditional loads, see ActStager
   auto load_w = [&](WFrag<BITS> (&w)[RT][NM], int64_t k) {
-    const int64_t kc = k < nst ? k * kStageK : 0;
+    const int64_t kc = (k < nst ? k : nst - 1) * kStageK;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
