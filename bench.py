@@ -371,6 +371,11 @@ def run_stack(args):
     prec = torch.empty((NL, T, K), dtype=torch.int8, device=dev)
     prefill = wl.mode == "prefill"
 
+    # decode stacks take the residual stream itself (moe_decode_step_prenorm:
+    # each layer forms its own input norm inside its router); --glue residual
+    # runs the separate norm kernel after every layer instead
+    prenorm = not prefill and args.glue == "prenorm"
+
     def step():
         h.copy_(h0)
         xb[0].copy_(x_first)
@@ -378,6 +383,8 @@ def run_stack(args):
             xi, xo = xb[l % 2], xb[(l + 1) % 2]
             if prefill:
                 L.prefill_residual(xi, h, xo, idx[l], gw[l], prec[l])
+            elif prenorm:
+                L.decode_step_prenorm(h, xi, idx[l], gw[l], prec[l])
             else:
                 L.decode_step_residual(xi, h, xo, idx[l], gw[l], prec[l])
 
@@ -471,7 +478,8 @@ def run_stack(args):
         "config": {"workload": wl.name, "d_model": d, "d_ff": wl.d_ff,
                    "n_experts": wl.n_experts, "top_k": K, "tokens_per_step": T,
                    "layers": NL, "mode": wl.mode, "tags": wl.note,
-                   "launch": "hipGraph replay of the whole pass" if graph is not None else "eager"},
+                   "launch": "hipGraph replay of the whole pass" if graph is not None else "eager",
+                   "glue": "prefill residual" if prefill else args.glue},
         "effective_weight_GBps": b / t_s / 1e9,
         "pct_hbm_peak": 100.0 * b / t_s / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": b, "flops_per_step": fl,
@@ -817,6 +825,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--cpu-tokens", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--glue", choices=("prenorm", "residual"), default="prenorm",
+                    help="decode stacks: residual RMSNorm formed by each layer's router "
+                         "(prenorm) or by a norm kernel after each layer (residual)")
     ap.add_argument("--graph", action="store_true",
                     help="stacks: replay one captured HIP graph per pass instead of launching each kernel")
     ap.add_argument("--pmc-pass", action="store_true",

@@ -170,6 +170,22 @@ moe_status moe_decode_step_residual(moe_layer_t layer, int32_t n_tokens,
                                     int32_t* topk_idx, float* topk_w,
                                     int8_t* prec_used, void* stream);
 
+/* Decode step of a stacked layer that takes the residual stream itself
+ * (Eq. 1 with the Section 3.2 rule inside the pre-norm residual glue):
+ *  h  device fp32 [n_tokens, d_model], in/out: on entry the residual
+ *     stream before this layer; the step forms x = fp16(rmsnorm(h)) (as
+ *     moe_rmsnorm), then h += MoE(x)
+ *  x  device fp16 [n_tokens, d_model], out: that x (the layer's input)
+ * A stack of layers is one call per layer on the same h; the results equal
+ * moe_rmsnorm followed by moe_decode_step_residual per layer, bit for bit,
+ * with one launch fewer per layer (the router forms the norm when the
+ * step's activations fit in its LDS: n_tokens * d_model <= 32768 and
+ * d_model <= 4096).  Other arguments, limits and errors as
+ * moe_decode_step. */
+moe_status moe_decode_step_prenorm(moe_layer_t layer, int32_t n_tokens, float* h,
+                                   void* x, int32_t* topk_idx, float* topk_w,
+                                   int8_t* prec_used, void* stream);
+
 /* Prefill: the same layer for 1 <= n_tokens <= max_tokens tokens, with the
  * experts run as an MFMA grouped GEMM.  Arguments as moe_decode_step. */
 moe_status moe_prefill(moe_layer_t layer, int32_t n_tokens, const void* x,

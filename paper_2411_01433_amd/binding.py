@@ -20,7 +20,8 @@ PREC_HIGH, PREC_LOW, PREC_SKIP = 0, 1, 2
 
 EXPORTED = (
     "moe_layer_init", "moe_set_expert_precision", "moe_decode_step",
-    "moe_decode_step_residual", "moe_prefill", "moe_prefill_residual",
+    "moe_decode_step_residual", "moe_decode_step_prenorm", "moe_prefill",
+    "moe_prefill_residual",
     "moe_export_packed", "moe_quantize", "moe_layer_enable_timing",
     "moe_layer_stage_times", "moe_layer_destroy", "moe_layer_share_workspace",
     "moe_last_error",
@@ -85,6 +86,7 @@ def lib() -> ctypes.CDLL:
     res = [vp, i32, vp, f32p, vp, vp, vp, vp, vp]
     L.moe_decode_step_residual.argtypes = res
     L.moe_prefill_residual.argtypes = res
+    L.moe_decode_step_prenorm.argtypes = [vp, i32, f32p, vp, vp, vp, vp, vp]
     L.moe_export_packed.argtypes = [vp, i32, i32, i32, vp, vp, vp]
     L.moe_quantize.argtypes = [vp, i64, i64, i32, vp, vp, vp]
     L.moe_layer_enable_timing.argtypes = [vp, i32]
@@ -241,6 +243,17 @@ class MoeLayer:
                              prec_used=None, stream=None):
         self._step_res(lib().moe_decode_step_residual, x, h, x_next, topk_idx,
                        topk_w, prec_used, stream)
+
+    def decode_step_prenorm(self, h, x, topk_idx=None, topk_w=None, prec_used=None,
+                            stream=None):
+        """moe_decode_step_prenorm: x = fp16(rmsnorm(h)) formed by the step, then
+        h += MoE(x) (h is the residual stream, x an output)."""
+        import torch
+        T = h.shape[0]
+        _check(lib().moe_decode_step_prenorm(
+            self._h, T, _ptr(h, torch.float32, (T, self.d), "h"),
+            _ptr(x, torch.float16, (T, self.d), "x"),
+            *self._outs(T, topk_idx, topk_w, prec_used), _stream(stream)))
 
     def prefill_residual(self, x, h, x_next, topk_idx=None, topk_w=None,
                          prec_used=None, stream=None):

@@ -59,29 +59,6 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
-// Sum over the 64 lanes of a wave in registers (every lane gets the sum):
-// butterflies inside each 16-lane row by DPP (lane ^ 1, lane ^ 2, mirror
-// in 8, mirror in 16), then the rows pairwise by v_permlane16_swap and the
-// halves by v_permlane32_swap.  __shfl_xor goes through LDS permutes
-// (ds_bpermute), about a hundred cycles per step.
-template <int CTRL>
-__device__ inline float dpp_f(float v) {
-  return __builtin_bit_cast(
-      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
-}
-__device__ inline float wave_sum_dpp(float v) {
-  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
-  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
-  v += dpp_f<0x141>(v);  // row_half_mirror
-  v += dpp_f<0x140>(v);  // row_mirror
-  const uint32_t u = __builtin_bit_cast(uint32_t, v);
-  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  v = __builtin_bit_cast(float, (uint32_t)r16[0]) + __builtin_bit_cast(float, (uint32_t)r16[1]);
-  const uint32_t w = __builtin_bit_cast(uint32_t, v);
-  const auto r32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
-  return __builtin_bit_cast(float, (uint32_t)r32[0]) + __builtin_bit_cast(float, (uint32_t)r32[1]);
-}
-
 // low half of a | low half of b  /  high half of a | high half of b
 __device__ inline uint32_t lo_lo(uint32_t a, uint32_t b) {
   return __builtin_amdgcn_perm(b, a, 0x05040100u);
@@ -518,48 +495,15 @@ __global__ __launch_bounds__(kThreads) void decode_down_kernel(
 }
 
 // ------------------------------------------------------ residual RMSNorm
-// One block of 1024 threads per token.  Each thread keeps its float4
-// pieces of the row in registers (d <= 16384: at most 4 per thread), so
-// h_res is read once; sum of squares per thread, over the wave in
-// registers, then over the 16 waves in a fixed order.
-constexpr int kNormThreads = 1024;
-constexpr int kNormPieces = 4;  // float4 pieces per thread: 16384 / (1024 * 4)
-
+// One block of 1024 threads per token (rmsnorm_rows in moe_internal.h).
 __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(
     const float* __restrict__ h_res, f16* __restrict__ x_next, int d, float eps) {
   __shared__ float red[kNormThreads / 64];
-  const int64_t base = (int64_t)blockIdx.x * d;
-  const f32x4* src = reinterpret_cast<const f32x4*>(h_res + base);
-  const int n4 = d >> 2;  // d is a multiple of 64
-  f32x4 v[kNormPieces];
-  float ss = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kNormPieces; ++i) {
-    const int q = threadIdx.x + i * kNormThreads;
-    v[i] = q < n4 ? src[q] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    ss = fmaf(v[i].x, v[i].x, ss);
-    ss = fmaf(v[i].y, v[i].y, ss);
-    ss = fmaf(v[i].z, v[i].z, ss);
-    ss = fmaf(v[i].w, v[i].w, ss);
-  }
-  ss = wave_sum_dpp(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  float tot = 0.0f;
-#pragma unroll
-  for (int w = 0; w < kNormThreads / 64; ++w) tot += red[w];
-  const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  f16* dst = x_next + base;
-#pragma unroll
-  for (int i = 0; i < kNormPieces; ++i) {
-    const int q = threadIdx.x + i * kNormThreads;
-    if (q < n4) {
-      const f16x2 lo = {(f16)(v[i].x * r), (f16)(v[i].y * r)};
-      const f16x2 hi = {(f16)(v[i].z * r), (f16)(v[i].w * r)};
-      *reinterpret_cast<u32x2*>(dst + 4 * q) =
-          u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-    }
-  }
+  rmsnorm_rows<1, kNormPieces>(h_res, d, eps, blockIdx.x, 1, red,
+                               [&](int t, int q, uint32_t lo, uint32_t hi) {
+                                 *reinterpret_cast<u32x2*>(x_next + (int64_t)t * d + 4 * q) =
+                                     u32x2{lo, hi};
+                               });
 }
 
 // The host takes these kernels for one or two tokens per step, and for up

@@ -190,14 +190,29 @@ bool decode_on_matrix_cores(int T, int K, int E) {
 
 // The launch sequence of a decode step with the workspace `ws` (the layer's
 // arena, or the static scratch of the allocation-free entry point).
+// With prenorm, h_res is the residual stream on entry and x an output: the
+// step forms x = fp16(rmsnorm(h_res)) first (inside the router when its
+// activations fit in its LDS, else with the norm kernel), then
+// h_res += MoE(x); x_next is not formed.
 moe_status decode_launch(moe_layer* l, const Workspace& ws, int32_t T, const void* x, float* y,
                          float* h_res, void* x_next, int32_t* idx, float* w, int8_t* prec,
-                         hipStream_t s) {
+                         hipStream_t s, bool prenorm = false) {
   const int d = l->desc.d_model, f = l->desc.d_ff, K = l->desc.top_k;
   const int mg = max_groups_of(l, T);
   HIP_TRY(mark(l, 0, s), "timing event");
-  HIP_TRY(launch_route_decode(route_params(l, T, x), route_out(ws, idx, w, prec),
-                              ws.wl, ws.perm, ws.pos, s), "route kernel launch");
+  RouteParams rp = route_params(l, T, x);
+  if (prenorm) {
+    if (route_decode_fuses_norm(T, d)) {
+      rp.h_res = h_res;
+      rp.x_out = static_cast<f16*>(const_cast<void*>(x));
+      rp.eps = l->desc.rms_eps;
+    } else {
+      HIP_TRY(launch_rmsnorm(h_res, static_cast<f16*>(const_cast<void*>(x)), T, d,
+                             l->desc.rms_eps, s), "rmsnorm kernel launch");
+    }
+  }
+  HIP_TRY(launch_route_decode(rp, route_out(ws, idx, w, prec), ws.wl, ws.perm, ws.pos, s),
+          "route kernel launch");
   HIP_TRY(mark(l, 1, s), "timing event");
   if (decode_on_matrix_cores(T, K, l->desc.n_experts)) {
     // several tokens per expert copy: matrix-core kernels, per-pair down
@@ -218,7 +233,7 @@ moe_status decode_launch(moe_layer* l, const Workspace& ws, int32_t T, const voi
     HIP_TRY(launch_decode_down(l->d_table, ws.wl, ws.perm, ws.w, ws.h, y, h_res,
                                T, d, f, K, s), "down kernel launch");
     HIP_TRY(mark(l, 3, s), "timing event");
-    if (h_res)
+    if (h_res && x_next)
       HIP_TRY(launch_rmsnorm(h_res, static_cast<f16*>(x_next), T, d, l->desc.rms_eps, s),
               "rmsnorm kernel launch");
   }
@@ -682,6 +697,19 @@ moe_status moe_decode_step_residual(moe_layer_t l, int32_t n_tokens, const void*
                                     float* topk_w, int8_t* prec_used, void* stream) {
   g_err.clear();
   return decode_impl(l, n_tokens, x, nullptr, h, x_next, topk_idx, topk_w, prec_used, stream);
+}
+
+moe_status moe_decode_step_prenorm(moe_layer_t l, int32_t T, float* h, void* x,
+                                   int32_t* topk_idx, float* topk_w, int8_t* prec_used,
+                                   void* stream) {
+  g_err.clear();
+  if (!l || !live(l)) return fail(MOE_ESTATE, "invalid or destroyed layer handle");
+  const int lim = l->desc.max_tokens < kDecodeMaxTokens ? l->desc.max_tokens : kDecodeMaxTokens;
+  moe_status st = check_call(l, T, lim, h, x, nullptr);
+  if (st != MOE_OK) return st;
+  if ((st = set_device(l)) != MOE_OK) return st;
+  return decode_launch(l, l->ws, T, x, nullptr, h, nullptr, topk_idx, topk_w, prec_used,
+                       static_cast<hipStream_t>(stream), true);
 }
 
 moe_status moe_prefill(moe_layer_t l, int32_t n_tokens, const void* x, float* y,

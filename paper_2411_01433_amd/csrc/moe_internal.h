@@ -57,6 +57,92 @@ struct WorkList {
   Group groups[kMaxKeys];
 };
 
+// ---- device helpers shared by several kernels ------------------------------
+
+// Sum over the 64 lanes of a wave in registers (every lane gets the sum):
+// butterflies inside each 16-lane row by DPP (lane ^ 1, lane ^ 2, mirror in
+// 8, mirror in 16), then the rows pairwise by v_permlane16_swap and the
+// halves by v_permlane32_swap.  __shfl_xor goes through LDS permutes
+// (ds_bpermute), about a hundred cycles per step.
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ inline float wave_sum_dpp(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror
+  v += dpp_f<0x140>(v);  // row_mirror
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  v = __builtin_bit_cast(float, (uint32_t)r16[0]) + __builtin_bit_cast(float, (uint32_t)r16[1]);
+  const uint32_t w = __builtin_bit_cast(uint32_t, v);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+  return __builtin_bit_cast(float, (uint32_t)r32[0]) + __builtin_bit_cast(float, (uint32_t)r32[1]);
+}
+
+// Residual RMSNorm of the residual glue, x = fp16(v / sqrt(mean(v^2) + eps)),
+// for rows t0 .. t0 + nb - 1 (nb <= NB) of h (fp32 [*, d], d a multiple of 64
+// and at most 4096 * PIECES), by one block of kNormThreads threads.  Thread i
+// holds float4 pieces i, i + 1024, ... of a row in registers (h is read
+// once) and sums their squares with fmaf in element order; the sum goes over
+// the wave in registers and then over the 16 waves in index order.  Every
+// caller forms the same sums in the same order, so x is bit-identical
+// whichever kernel computes it (pieces past the row add exact zeros).
+// store(t, q, lo, hi) receives piece q of row t as two fp16 pairs.  `red`:
+// NB * 16 floats of LDS.  Ends with a barrier (red may be reused).
+constexpr int kNormThreads = 1024;
+constexpr int kNormPieces = 4;  // float4 pieces per thread: 16384 / (1024 * 4)
+
+template <int NB, int PIECES, class Store>
+__device__ inline void rmsnorm_rows(const float* __restrict__ h, int d, float eps, int t0,
+                                    int nb, float* red, Store store) {
+  const int n4 = d >> 2;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  f32x4 v[NB][PIECES];
+  float ss[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    ss[b] = 0.0f;
+    const f32x4* src = reinterpret_cast<const f32x4*>(h + (int64_t)(t0 + (b < nb ? b : 0)) * d);
+#pragma unroll
+    for (int i = 0; i < PIECES; ++i) {
+      const int q = threadIdx.x + i * kNormThreads;
+      v[b][i] = (b < nb && q < n4) ? src[q] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      ss[b] = fmaf(v[b][i].x, v[b][i].x, ss[b]);
+      ss[b] = fmaf(v[b][i].y, v[b][i].y, ss[b]);
+      ss[b] = fmaf(v[b][i].z, v[b][i].z, ss[b]);
+      ss[b] = fmaf(v[b][i].w, v[b][i].w, ss[b]);
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const float s = wave_sum_dpp(ss[b]);
+    if (lane == 0) red[b * (kNormThreads / 64) + wave] = s;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    if (b < nb) {
+      float tot = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kNormThreads / 64; ++w) tot += red[b * (kNormThreads / 64) + w];
+      const float r = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+      for (int i = 0; i < PIECES; ++i) {
+        const int q = threadIdx.x + i * kNormThreads;
+        if (q < n4) {
+          const f16x2 lo = {(f16)(v[b][i].x * r), (f16)(v[b][i].y * r)};
+          const f16x2 hi = {(f16)(v[b][i].z * r), (f16)(v[b][i].w * r)};
+          store(t0 + b, q, __builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
 // Device workspace of one layer call: the work list, the pair permutation
 // and its inverse, the routing outputs, the SwiGLU activations h of every
 // pair and the per-pair expert outputs (prefill and matrix-core decode).
@@ -83,6 +169,11 @@ struct RouteOut {
 
 struct RouteParams {
   const f16* x;         // [T, d]
+  // decode router only: with h_res set, the router forms x itself as
+  // fp16(rmsnorm(h_res)) (eps), writes it to x_out and routes it
+  const float* h_res = nullptr;   // [T, d]
+  f16* x_out = nullptr;           // [T, d]
+  float eps = 0.0f;
   const f16* wg;        // [E, d]
   const ExpertEntry* table;
   int32_t T, d, E, K;
@@ -119,6 +210,9 @@ hipError_t launch_set_entry(ExpertEntry* table, int e, ExpertEntry v,
                             hipStream_t s);
 hipError_t launch_route_decode(const RouteParams& p, RouteOut o, WorkList* wl,
                                int32_t* perm, int32_t* pos, hipStream_t s);
+// Whether the decode router can form the RMSNorm of h_res itself for T
+// tokens of d_model d (its activations then fit in its LDS).
+bool route_decode_fuses_norm(int T, int d);
 hipError_t launch_route_prefill(const RouteParams& p, RouteOut o, WorkList* wl,
                                 int32_t* perm, int32_t* pos, hipStream_t s);
 hipError_t launch_decode_up(const ExpertEntry* table, const WorkList* wl,

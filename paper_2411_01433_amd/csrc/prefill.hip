@@ -501,17 +501,13 @@ __global__ __launch_bounds__(kThreads, RT == 2 ? 1 : 2) void prefill_down_kernel
   else down_group<2, RT>(ex, g, h, e, d, f, tile, lds);
 }
 
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
+// One block per token; thread i owns the float4 pieces i, i + 1024, ... of
+// the token's row (d is a multiple of 64): y[t] = sum_k w[t,k] *
+// E[pos(t,k)] in slot order (skip -> 0); with h_res: h_res[t] += that and,
+// with x_next, x_next[t] = fp16(rmsnorm(h_res[t])) by rmsnorm_rows (the
+// same piece layout, so each thread reads back the pieces it wrote).
+constexpr int kCombineThreads = kNormThreads;
 
-constexpr int kCombineThreads = 512;
-
-// y[t] = sum_k w[t,k] * E[pos(t,k)] in slot order (skip -> 0); with h_res:
-// h_res[t] += that and x_next[t] = fp16(rmsnorm(h_res[t])).  One block per
-// token, 4 columns per thread per step (d is a multiple of 64).
 __global__ __launch_bounds__(kCombineThreads) void combine_prefill_kernel(
     const float* __restrict__ e, const int32_t* __restrict__ pos,
     const float* __restrict__ w, const int8_t* __restrict__ prec, int d, int K,
@@ -528,36 +524,31 @@ __global__ __launch_bounds__(kCombineThreads) void combine_prefill_kernel(
   }
   __syncthreads();
   const int64_t base = (int64_t)t * d;
-  float ss = 0.0f;
-  for (int c = threadIdx.x * 4; c < d; c += kCombineThreads * 4) {
-    f32x4 acc = {0, 0, 0, 0};
-    for (int k = 0; k < K; ++k)
-      if (s_pos[k] >= 0) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(e + (int64_t)s_pos[k] * d + c);
-        acc += s_w[k] * v;
+  const int n4 = d >> 2;
+#pragma unroll
+  for (int i = 0; i < kNormPieces; ++i) {
+    const int q = threadIdx.x + i * kCombineThreads;
+    if (q < n4) {
+      const int c = 4 * q;
+      f32x4 acc = {0, 0, 0, 0};
+      for (int k = 0; k < K; ++k)
+        if (s_pos[k] >= 0) {
+          const f32x4 v = *reinterpret_cast<const f32x4*>(e + (int64_t)s_pos[k] * d + c);
+          acc += s_w[k] * v;
+        }
+      if (h_res) {
+        f32x4* hp = reinterpret_cast<f32x4*>(h_res + base + c);
+        *hp = *hp + acc;
+      } else {
+        *reinterpret_cast<f32x4*>(y + base + c) = acc;
       }
-    if (h_res) {
-      f32x4 hv = *reinterpret_cast<const f32x4*>(h_res + base + c) + acc;
-      *reinterpret_cast<f32x4*>(h_res + base + c) = hv;
-      ss += hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w;
-    } else {
-      *reinterpret_cast<f32x4*>(y + base + c) = acc;
     }
   }
-  if (!h_res) return;
-  ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  float tot = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kCombineThreads / 64; ++i) tot += red[i];
-  const float r = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x * 4; c < d; c += kCombineThreads * 4) {
-    const f32x4 hv = *reinterpret_cast<const f32x4*>(h_res + base + c);
-    f16x4 o;
-    o[0] = (f16)(hv.x * r); o[1] = (f16)(hv.y * r); o[2] = (f16)(hv.z * r); o[3] = (f16)(hv.w * r);
-    *reinterpret_cast<f16x4*>(x_next + base + c) = o;
-  }
+  if (!h_res || !x_next) return;  // no norm asked for (the next layer forms it)
+  rmsnorm_rows<1, kNormPieces>(h_res + base, d, eps, 0, 1, red,
+                               [&](int, int q, uint32_t lo, uint32_t hi) {
+                                 *reinterpret_cast<u32x2*>(x_next + base + 4 * q) = u32x2{lo, hi};
+                               });
 }
 
 }  // namespace

@@ -29,27 +29,8 @@ __device__ inline float dot2(uint32_t a, uint32_t b, float acc) {
                                 __builtin_bit_cast(f16x2, b), acc, false);
 }
 
-// Sum over the 64 lanes of a wave in registers (every lane gets the sum):
-// DPP butterflies inside each 16-lane row, then v_permlane16_swap and
-// v_permlane32_swap across rows.  The decode and prefill routers both sum
-// their logits with it, so their logits stay bit-identical.
-template <int CTRL>
-__device__ inline float dpp_f(float v) {
-  return __builtin_bit_cast(
-      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
-}
-__device__ inline float wave_sum(float v) {
-  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
-  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
-  v += dpp_f<0x141>(v);  // row_half_mirror
-  v += dpp_f<0x140>(v);  // row_mirror
-  const uint32_t u = __builtin_bit_cast(uint32_t, v);
-  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  v = __builtin_bit_cast(float, (uint32_t)r16[0]) + __builtin_bit_cast(float, (uint32_t)r16[1]);
-  const uint32_t w = __builtin_bit_cast(uint32_t, v);
-  const auto r32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
-  return __builtin_bit_cast(float, (uint32_t)r32[0]) + __builtin_bit_cast(float, (uint32_t)r32[1]);
-}
+// Wave sums use wave_sum_dpp (moe_internal.h): the decode and prefill
+// routers sum their logits with it, so their logits stay bit-identical.
 
 // Dot products of tokens [t0, t1) against all E gate rows.  One wave per
 // (expert, batch of up to TB tokens): the gate row chunk is loaded once and
@@ -96,7 +77,7 @@ __device__ void gate_logits(const RouteParams& p, int t0, int t1, float* lg) {
     }
 #pragma unroll
     for (int i = 0; i < TB; ++i) {
-      const float v = wave_sum(acc[i]);
+      const float v = wave_sum_dpp(acc[i]);
       if (lane == 0 && i < nt) lg[(tb0 - t0 + i) * p.E + e] = v;
     }
   }
@@ -284,6 +265,10 @@ struct TableRow {
 // gate_logits, so the logits are bit-identical to the other routers'.
 constexpr int kFastXBytes = 64 * 1024;
 constexpr int kFastChunks = 8;  // 512-column chunks held in registers at once
+constexpr int kNormBatch = 4;   // tokens per round of the fused RMSNorm
+static_assert(kRouteThreads == kNormThreads, "the fused RMSNorm runs on the whole router block");
+
+__host__ __device__ inline bool fast_gate(int T, int d) { return (int64_t)T * d * 2 <= kFastXBytes && d <= kFastChunks * 512; }
 
 __device__ void gate_fast(const RouteParams& p, f16* xs, float* lg) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -299,10 +284,24 @@ __device__ void gate_fast(const RouteParams& p, f16* xs, float* lg) {
                ? *reinterpret_cast<const u32x4*>(p.wg + (int64_t)e0 * p.d + c)
                : u32x4{0, 0, 0, 0};
   }
-  // stage x [T, d] in LDS
-  const int nvec = p.T * p.d / 8;
-  for (int v = threadIdx.x; v < nvec; v += kRouteThreads)
-    reinterpret_cast<u32x4*>(xs)[v] = reinterpret_cast<const u32x4*>(p.x)[v];
+  if (p.h_res) {
+    // x = fp16(rmsnorm(h_res)), formed here as the residual glue's norm
+    // kernel forms it (same sums, same order: bit-identical), written to
+    // x_out for the expert kernels and staged in LDS for the gate
+    __shared__ float red[kNormBatch * (kNormThreads / 64)];
+    for (int t0 = 0; t0 < p.T; t0 += kNormBatch)
+      rmsnorm_rows<kNormBatch, 1>(p.h_res, p.d, p.eps, t0, min(kNormBatch, p.T - t0), red,
+                                  [&](int t, int q, uint32_t lo, uint32_t hi) {
+                                    const int64_t o = (int64_t)t * p.d + 4 * q;
+                                    *reinterpret_cast<u32x2*>(p.x_out + o) = u32x2{lo, hi};
+                                    *reinterpret_cast<u32x2*>(xs + o) = u32x2{lo, hi};
+                                  });
+  } else {
+    // stage x [T, d] in LDS
+    const int nvec = p.T * p.d / 8;
+    for (int v = threadIdx.x; v < nvec; v += kRouteThreads)
+      reinterpret_cast<u32x4*>(xs)[v] = reinterpret_cast<const u32x4*>(p.x)[v];
+  }
   __syncthreads();
   for (int e = e0; e < p.E; e += kW) {
     if (e != e0) {
@@ -326,7 +325,7 @@ __device__ void gate_fast(const RouteParams& p, f16* xs, float* lg) {
           acc = dot2(xv.w, b[j].w, acc);
         }
       }
-      const float v = wave_sum(acc);
+      const float v = wave_sum_dpp(acc);
       if (lane == 0) lg[t * p.E + e] = v;
     }
   }
@@ -459,7 +458,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_decode_kernel(
   __shared__ __attribute__((aligned(16))) f16 xs[kFastXBytes / 2];
   TableRow tr;
   tr.load(p);
-  const bool fast = (int64_t)p.T * p.d * 2 <= kFastXBytes && p.d <= kFastChunks * 512;
+  const bool fast = fast_gate(p.T, p.d);
   if (fast) gate_fast(p, xs, lg);
   else if (p.T == 1) gate_logits<1, 8>(p, 0, p.T, lg);
   else if (p.T == 2) gate_logits<2, 8>(p, 0, p.T, lg);
@@ -499,8 +498,12 @@ __global__ __launch_bounds__(kRouteThreads) void worklist_kernel(
 
 }  // namespace
 
+bool route_decode_fuses_norm(int T, int d) { return fast_gate(T, d); }
+
 hipError_t launch_route_decode(const RouteParams& p, RouteOut o, WorkList* wl,
                                int32_t* perm, int32_t* pos, hipStream_t s) {
+  // the fused RMSNorm exists on the LDS-staged gate path only
+  if (p.h_res && !fast_gate(p.T, p.d)) return hipErrorInvalidValue;
   route_decode_kernel<<<1, kRouteThreads, 0, s>>>(p, o, wl, perm, pos);
   return hipGetLastError();
 }

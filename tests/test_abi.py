@@ -94,6 +94,7 @@ def test_calls_on_invalid_handles_fail_cleanly():
     assert L.moe_decode_step(bogus, 1, x, x, None, None, None, None) == B.MOE_ESTATE
     assert L.moe_prefill(bogus, 1, x, x, None, None, None, None) == B.MOE_ESTATE
     assert L.moe_decode_step_residual(bogus, 1, x, x, x, None, None, None, None) == B.MOE_ESTATE
+    assert L.moe_decode_step_prenorm(bogus, 1, x, x, None, None, None, None) == B.MOE_ESTATE
     assert L.moe_prefill_residual(bogus, 1, x, x, x, None, None, None, None) == B.MOE_ESTATE
     assert L.moe_export_packed(bogus, 0, 0, 4, x, x, None) == B.MOE_ESTATE
     assert L.moe_layer_destroy(bogus) == B.MOE_ESTATE
