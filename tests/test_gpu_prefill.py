@@ -106,6 +106,23 @@ def test_prefill_skip_and_residual():
     _check(wl, wl.fixed_tags, x, t1=0.0, t2=1.0)
 
 
+def test_prefill_max_tokens():
+    """The largest step a layer takes (8192 tokens): about 2,000 tokens per
+    group, i.e. 13 passes of 160 tokens per weight tile, every tag kind;
+    routing of all tokens, the output on 512 evenly spread tokens."""
+    T = 8192
+    wl = _edge("prefill_max", 44, 256, 512, 8, 2, T,
+               [C.TAG_FP16, C.TAG_INT4, C.TAG_INT2, C.TAG_MISS_INT4, C.TAG_MISS_INT2,
+                C.TAG_FP16, C.TAG_MISS_INT4, C.TAG_INT4], t1=0.3, t2=0.6)
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((T, 256)).astype(np.float16)
+    idx, prec = _check(wl, wl.fixed_tags, x, sample=np.linspace(0, T - 1, 512).astype(int))
+    counts = np.bincount(idx.ravel(), minlength=8)
+    assert counts.min() > 160, counts
+    # all three outcomes of Eq. 2 occur on the miss-tagged experts
+    assert {0, 1, 2} <= set(np.unique(prec).tolist()), np.unique(prec)
+
+
 def test_prefill_mixtral_layer_t512():
     """One Mixtral-shaped layer of the 512-token prefill workload (4:3:1
     map of layer 0): routing of all 512 tokens, the layer output on 32
