@@ -98,20 +98,21 @@ def measured_traffic(workload):
     return b, "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
 
 
-def event_overhead_us(n=50):
+def event_overhead_us(n=50, warm=10):
     """Cost of two HIP event records back to back after a kernel on the
     current stream (what an empty stage of the library's stage timing
-    measures)."""
+    measures): the median of n pairs after `warm` untimed ones (single
+    pairs occasionally read several times the typical value)."""
     import torch
     a = torch.zeros(256, device="cuda")
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(n)]
+             for _ in range(warm + n)]
     for e0, e1 in pairs:
         a.add_(1.0)
         e0.record()
         e1.record()
     torch.cuda.synchronize()
-    return float(np.mean([e0.elapsed_time(e1) for e0, e1 in pairs]) * 1e3)
+    return float(np.median([e0.elapsed_time(e1) for e0, e1 in pairs[warm:]]) * 1e3)
 
 
 def log(*a):
